@@ -1,0 +1,192 @@
+"""Throughput of the FP8 linear-layer hot path on one MI355X.
+
+One step = quantize the activations X[16384, 4096] per 1x128 block, quantize
+the weights W[12288, 4096] per 128x128 block, and run the blockwise scaled
+FP8 GEMM Y = X W^T (8B-class FFN up-projection, one 16K-token sequence;
+paper Sec. 2.2, Eq. 3, and the FP8 training engine of Sec. 5.3).  Inputs are
+seeded synthetic bf16 tensors resident in HBM before timing starts.
+
+Prints one JSON line: value = GEMM flops (2 M N K) per step time in TFLOP/s,
+plus the roofline of the dominant kernel (the GEMM, timed with HIP events on
+its stream) and the oracle's CPU throughput on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP8_TFLOPS = 5000.0   # MI355X dense FP8 MFMA
+PEAK_HBM_GBS = 8000.0      # MI355X HBM3E
+
+WORKLOADS = {
+    "8b_ffn_up_fwd_blockwise": (16384, 4096, 12288),
+}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="8b_ffn_up_fwd_blockwise", choices=sorted(WORKLOADS))
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=256,
+                   help="rows of X the oracle processes for the CPU baseline")
+    return p.parse_args()
+
+
+def cpu_baseline(x, w, M, K, N, rows):
+    """The oracle (untuned) on a sample of the same step: `rows` rows of X
+    quantized 1x128, the matching share of W's rows (rounded up to whole
+    128-row blocks) quantized 128x128, and those rows of Y computed exactly.
+    Runs on all host cores, one oracle call per thread."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle
+    from paper_2609_22870_amd import synth
+
+    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    xs = synth.bf16_bits(x[:rows])
+    wrows = max(128, ((N * rows // M + 127) // 128) * 128)
+    wb = synth.bf16_bits(w)
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(cores) as ex:
+        xparts = np.array_split(np.arange(rows), cores)
+        xres = list(ex.map(lambda r: oracle.quantize(xs[r[0]:r[-1] + 1], oracle.BLOCK_1x128), xparts))
+        wblocks = [(i, min(wrows, i + 128)) for i in range(0, wrows, 128)]
+        list(ex.map(lambda ab: oracle.quantize(wb[ab[0]:ab[1]], oracle.BLOCK_128x128), wblocks))
+    t_quant = time.perf_counter() - t0
+    # the GEMM rows need W quantized whole; that is not timed again (the W
+    # share above already stands for it at the sampled rate)
+    with ThreadPoolExecutor(cores) as ex:
+        wparts = list(ex.map(lambda i: oracle.quantize(wb[i:i + 128], oracle.BLOCK_128x128),
+                             range(0, N, 128)))
+    ow = np.concatenate([c for c, _ in wparts])
+    osw = np.concatenate([s for _, s in wparts])
+    t1 = time.perf_counter()
+    with ThreadPoolExecutor(cores) as ex:
+        def rows_of(i):
+            codes, scales = xres[i]
+            n = codes.shape[0]
+            return oracle.gemm_rows(codes, scales, oracle.BLOCK_1x128, ow, osw,
+                                    oracle.BLOCK_128x128, np.arange(n))
+        list(ex.map(rows_of, range(len(xres))))
+    t_gemm = time.perf_counter() - t1
+    # the sampled share of one step: rows/M of the GEMM and of X, wrows/N of W
+    t_step = t_gemm + t_quant
+    flops = 2.0 * rows * N * K
+    return {
+        "value": flops / t_step / 1e12,
+        "unit": "TFLOP/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": "%d of %d rows of Y = X W^T (exact int64/binary128 oracle GEMM), "
+                  "those rows of X quantized 1x128 and %d of %d rows of W quantized "
+                  "128x128; %.1f s wall (%.1f s quantize, %.1f s GEMM)"
+                  % (rows, M, wrows, N, t_step, t_quant, t_gemm),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_22870_amd as fp8q
+    from paper_2609_22870_amd import synth
+
+    M, K, N = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    x = synth.activations(M, K, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=dev)
+    w = synth.weights(N, K, seed=synth.seed_for(2, 1), device=dev)
+    xq = torch.empty((M, K), dtype=torch.uint8, device=dev)
+    wq = torch.empty((N, K), dtype=torch.uint8, device=dev)
+    sx = torch.empty(fp8q.scales_count(M, K, fp8q.BLOCK_1x128), dtype=torch.float32, device=dev)
+    sw = torch.empty(fp8q.scales_count(N, K, fp8q.BLOCK_128x128), dtype=torch.float32, device=dev)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        fp8q.quantize(x, fp8q.BLOCK_1x128, codes=xq, scales=sx)
+        if ev is not None:
+            ev[1].record(stream)
+        fp8q.quantize(w, fp8q.BLOCK_128x128, codes=wq, scales=sw)
+        if ev is not None:
+            ev[2].record(stream)
+        fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y)
+        if ev is not None:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        step(events[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = start.elapsed_time(end) / args.steps
+
+    qx_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
+    qw_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
+    gemm_ms = sum(e[2].elapsed_time(e[3]) for e in events) / args.steps
+
+    flops = 2.0 * M * N * K
+    value = flops / (ms_step * 1e-3) / 1e12
+    gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    qx_bytes = 3.0 * M * K + 4.0 * M * (K // 128)
+    qw_bytes = 3.0 * N * K + 4.0 * (N // 128) * (K // 128)
+    out = {
+        "metric": "FP8 blockwise GEMM TFLOP/s and % of dense FP8 MFMA peak, 8B-class shapes",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8_e4m3",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "M": M, "K": K, "N": N,
+                   "scaling": "1x128 activation blocks, 128x128 weight blocks",
+                   "step": "quantize X + quantize W + blockwise FP8 GEMM"},
+        "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
+                     "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4),
+                     "traffic": None},
+        "pct_of_fp8_peak_step": round(100 * value / PEAK_FP8_TFLOPS, 2),
+        "kernels_ms": {"quantize_x_1x128": round(qx_ms, 4), "quantize_w_128x128": round(qw_ms, 4),
+                       "gemm_blockwise": round(gemm_ms, 4)},
+        "quantize_gbs": {"x_1x128": round(qx_bytes / (qx_ms * 1e-3) / 1e9, 1),
+                         "w_128x128": round(qw_bytes / (qw_ms * 1e-3) / 1e9, 1),
+                         "hbm_peak": PEAK_HBM_GBS},
+        "timed_wall_s": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(x.cpu(), w.cpu(), M, K, N, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,144 @@
+/*
+ * fp8q — FP8 scaled quantization and the scaled FP8 GEMM of an FP8 linear
+ * layer, for AMD Instinct MI355X (gfx950).
+ *
+ * The method (paper "Towards Full Pipeline FP8 Reinforcement Learning for
+ * LLMs", Sec. 2.2, Eq. 3): for a high-precision tensor X and a scaling unit
+ * U (the whole tensor, one row, or one block),
+ *     S_U = max_{x in U} |x| / F_max,  X_hat = Q_FP8(X / S_U),  X_tilde = S_U X_hat
+ * where Q_FP8 rounds and clamps to the FP8 set.  The FP8 training engine the
+ * paper uses (Sec. 5, experimental setup; Sec. 5.3, training throughput) runs
+ * the linear layers of the policy as GEMMs on such operands.
+ *
+ * Conventions fixed by this library:
+ *   - FP8 is OCP E4M3 (1.4.3, bias 7, no infinities, NaN = S.1111.111),
+ *     F_max = 448.  Codes are the raw E4M3 bytes.
+ *   - S is fp32: S = RN32(amax / 448), and S = 1 when that is 0.  `scales`
+ *     always holds S itself (the dequantization multiplier), never 1/S.
+ *   - Q_FP8(X / S) = E4M3 nearest-even of the correctly rounded fp32
+ *     quotient; magnitudes above 448 clamp to 448; the sign of zero is kept;
+ *     fp32 subnormals are not flushed.
+ *   - Inputs are bf16, row-major; Inf/NaN inputs are outside the contract.
+ *
+ * All data pointers are DEVICE pointers owned by the caller.  The library
+ * never allocates, frees or synchronizes; every call enqueues its kernels on
+ * `stream` (a hipStream_t; NULL is the legacy default stream) and returns.
+ * Arguments are validated on the host before anything is enqueued; a
+ * rejected call enqueues nothing.  Faults inside kernels surface at the
+ * caller's next synchronization.  The library holds no mutable global
+ * state, so calls from several threads are safe; calls that write the same
+ * buffers must be ordered by the caller.
+ */
+#ifndef FP8Q_H
+#define FP8Q_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+struct ihipStream_t; /* hipStream_t is `struct ihipStream_t *` */
+
+typedef enum {
+  FP8Q_OK = 0,
+  FP8Q_ERR_INVAL = -1,       /* null pointer, size <= 0, ld too small, bad enum */
+  FP8Q_ERR_UNSUPPORTED = -2, /* shape or granularity pair the kernels do not take */
+  FP8Q_ERR_ALIGN = -3,       /* pointer or leading dimension misaligned */
+  FP8Q_ERR_HIP = -4          /* a HIP launch failed */
+} fp8q_status;
+
+/* Scaling units of Eq. 3 (Sec. 2.2: tensorwise, rowwise, blockwise).
+ * They are stated on the INPUT matrix x[rows][cols]. */
+typedef enum {
+  FP8Q_TENSOR = 0,       /* one unit: the whole tensor                     */
+  FP8Q_ROW = 1,          /* one unit per row (per token / per out channel) */
+  FP8Q_COL = 2,          /* one unit per column                            */
+  FP8Q_BLOCK_1x128 = 3,  /* 128 consecutive elements of one row            */
+  FP8Q_BLOCK_128x1 = 4,  /* 128 consecutive elements of one column         */
+  FP8Q_BLOCK_128x128 = 5 /* 128 x 128 tiles                                */
+} fp8q_granularity;
+
+/* Write codes as the transpose, codes[c][r] = Q(x[r][c]).  The scaling
+ * units stay the same sets of elements; the scales are laid out for the
+ * transposed matrix (so 1x128 of x is 128x1 of x^T, ROW of x is COL). */
+enum { FP8Q_OUT_TRANSPOSED = 1u };
+
+/*
+ * Number of fp32 scales fp8q_quantize writes for an input of rows x cols
+ * with granularity g and `flags`; -1 if the arguments are invalid.
+ *
+ * Scale layouts, for the OUTPUT matrix o[orows][ocols] (x, or x^T when
+ * transposed) and the granularity g_o it sees (g, or g with rows and
+ * columns exchanged when transposed):
+ *   TENSOR   [1]
+ *   ROW      [orows]
+ *   COL      [ocols]
+ *   1x128    [ocols/128][orows]  block-column major: all rows of one
+ *                                128-wide column block are contiguous
+ *   128x1    [orows/128][ocols]
+ *   128x128  [orows/128][ocols/128]
+ * With these layouts the transposed output of 1x128 / 128x1 / ROW / COL /
+ * TENSOR uses the same scale array as the plain output; 128x128 transposes
+ * its block grid.
+ */
+int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g,
+                          unsigned flags);
+
+/*
+ * Eq. 3 per scaling unit: codes and scales of x.
+ *   x       bf16 [rows][ldx], ldx >= cols
+ *   codes   E4M3 [rows][ldc] (ldc >= cols), or [cols][ldc] (ldc >= rows)
+ *           with FP8Q_OUT_TRANSPOSED
+ *   scales  fp32, fp8q_scales_count(rows, cols, g, flags) entries
+ * Shape rules: cols % 16 == 0, and rows % 16 == 0 when transposed; a
+ * dimension a 128-block splits (cols for 1x128 and 128x128, rows for 128x1
+ * and 128x128) must be a multiple of 128 (else FP8Q_ERR_UNSUPPORTED).
+ * Alignment: x and codes 16-byte aligned, ldx % 8 == 0, ldc % 16 == 0,
+ * scales 4-byte aligned (else FP8Q_ERR_ALIGN).
+ * TENSOR, ROW and COL use `scales` as their amax scratch between kernels.
+ */
+fp8q_status fp8q_quantize(const void *x, int64_t rows, int64_t cols,
+                          int64_t ldx, fp8q_granularity g, unsigned flags,
+                          uint8_t *codes, int64_t ldc, float *scales,
+                          struct ihipStream_t *stream);
+
+/*
+ * The FP8 linear layer's GEMM on dequantized operands (Eq. 3 applied to
+ * both; fp32 accumulation; bf16 round-to-nearest-even output):
+ *   C[m][n] = sum_k (S_A(m,k) A[m][k]) (S_B(n,k) B[n][k])
+ *   A  E4M3 [M][lda], K contiguous (activations X, dY, or X^T / dY^T)
+ *   B  E4M3 [N][ldb], K contiguous (weights W stored [N][K], W^T, or dY^T)
+ *   C  bf16 [M][ldc]
+ * Forward Y = X W^T, dgrad dX = dY W and wgrad dW = dY^T X all take this
+ * form once the quantizer has written the operands K-contiguous (dgrad's W^T
+ * and wgrad's X^T, dY^T come from FP8Q_OUT_TRANSPOSED).
+ * Scales sA, sB in the layouts of fp8q_scales_count for A[M][K], B[N][K].
+ * Supported (gA, gB): (TENSOR, TENSOR), (ROW, ROW) — per-token x
+ * per-output-channel —, (1x128, 128x128) — activation blocks x weight
+ * blocks — and (1x128, 1x128) — both grouped along K, for wgrad.
+ * Shape rules: K % 128 == 0; N % 128 == 0 when gB is 128x128; M and N are
+ * otherwise free.  Alignment: A and B 16-byte aligned, lda % 16 == 0,
+ * ldb % 16 == 0; C 8-byte aligned with ldc % 4 == 0; scales 4-byte aligned.
+ */
+fp8q_status fp8q_gemm(const uint8_t *A, const float *sA, fp8q_granularity gA,
+                      int64_t lda, const uint8_t *B, const float *sB,
+                      fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N,
+                      int64_t K, void *C, int64_t ldc,
+                      struct ihipStream_t *stream);
+
+/*
+ * Q_FP8(RN32(x[i] / scale)) for n fp32 values with one explicit scale: the
+ * device rounding routine of fp8q_quantize exposed for exhaustive checks.
+ * x and codes need no alignment beyond their element size; scale > 0.
+ */
+fp8q_status fp8q_cast_f32(const float *x, int64_t n, float scale,
+                          uint8_t *codes, struct ihipStream_t *stream);
+
+/* Static string naming a status. */
+const char *fp8q_status_string(fp8q_status status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FP8Q_H */

@@ -1,0 +1,144 @@
+"""fp8q: FP8 scaled quantization (paper Sec. 2.2, Eq. 3) and the scaled FP8
+GEMM of the FP8 linear layer, as hand-written HIP kernels for MI355X (gfx950).
+
+This module is a thin ctypes binding over the C-ABI of ``libfp8q.so``
+(declared in ``include/fp8q.h``): it only marshals arguments.  PyTorch is
+used for device memory and the current HIP stream; every step of the
+computation runs in the library's kernels.  There is no fallback: if the
+library is missing, every call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfp8q.so")
+
+# fp8q_granularity
+TENSOR, ROW, COL, BLOCK_1x128, BLOCK_128x1, BLOCK_128x128 = range(6)
+OUT_TRANSPOSED = 1
+_STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
+           -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
+# the entry points of include/fp8q.h
+EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_gemm", "fp8q_cast_f32",
+           "fp8q_status_string")
+
+
+class Fp8qError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__("%s: %s" % (what, status_string(status)))
+
+
+_lib = None
+
+
+def lib():
+    """Load libfp8q.so (built by __graft_entry__.build()); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError("libfp8q.so is not built (%s); run "
+                              "__graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        p, i64, i32, u32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint
+        L.fp8q_scales_count.argtypes = [i64, i64, i32, u32]
+        L.fp8q_scales_count.restype = i64
+        L.fp8q_quantize.argtypes = [p, i64, i64, i64, i32, u32, p, i64, p, p]
+        L.fp8q_quantize.restype = i32
+        L.fp8q_gemm.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
+                                p, i64, p]
+        L.fp8q_gemm.restype = i32
+        L.fp8q_cast_f32.argtypes = [p, i64, ctypes.c_float, p, p]
+        L.fp8q_cast_f32.restype = i32
+        L.fp8q_status_string.argtypes = [i32]
+        L.fp8q_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def status_string(status):
+    try:
+        return lib().fp8q_status_string(status).decode()
+    except ImportError:
+        return _STATUS.get(status, str(status))
+
+
+def _check(status, what):
+    if status != 0:
+        raise Fp8qError(status, what)
+
+
+def _stream(t):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ld(t):
+    """Leading dimension of a row-major 2-D tensor (unit column stride)."""
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a row-major 2-D tensor")
+    return t.stride(0)
+
+
+def scales_count(rows, cols, granularity, transposed=False):
+    n = lib().fp8q_scales_count(rows, cols, granularity,
+                                OUT_TRANSPOSED if transposed else 0)
+    if n < 0:
+        raise ValueError("invalid quantization shape or granularity")
+    return n
+
+
+def quantize(x, granularity, transposed=False, codes=None, scales=None):
+    """Eq. 3 per scaling unit on a bf16 CUDA tensor x[rows, cols].
+
+    Returns (codes, scales): codes uint8 (OCP E4M3 bytes) [rows, cols], or
+    [cols, rows] when `transposed`; scales fp32 1-D in the layout of
+    include/fp8q.h.
+    """
+    if x.dtype != torch.bfloat16 or not x.is_cuda:
+        raise ValueError("x must be a bf16 CUDA tensor")
+    rows, cols = x.shape
+    oshape = (cols, rows) if transposed else (rows, cols)
+    if codes is None:
+        codes = torch.empty(oshape, dtype=torch.uint8, device=x.device)
+    if scales is None:
+        scales = torch.empty(scales_count(rows, cols, granularity, transposed),
+                             dtype=torch.float32, device=x.device)
+    st = lib().fp8q_quantize(x.data_ptr(), rows, cols, _ld(x), granularity,
+                             OUT_TRANSPOSED if transposed else 0,
+                             codes.data_ptr(), _ld(codes), scales.data_ptr(),
+                             _stream(x))
+    _check(st, "fp8q_quantize")
+    return codes, scales
+
+
+def gemm(a, sa, ga, b, sb, gb, out=None):
+    """C[M, N] = dequant(a)[M, K] @ dequant(b)[N, K]^T in bf16.
+
+    a, b: uint8 E4M3 codes, K contiguous; sa, sb: fp32 scales for the
+    granularities ga, gb (pairs listed in include/fp8q.h).
+    """
+    M, K = a.shape
+    N, K2 = b.shape
+    if K != K2:
+        raise ValueError("contraction sizes differ")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    st = lib().fp8q_gemm(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
+                         b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
+                         out.data_ptr(), _ld(out), _stream(a))
+    _check(st, "fp8q_gemm")
+    return out
+
+
+def cast_f32(x, scale, codes=None):
+    """Q_FP8(RN32(x / scale)) elementwise on an fp32 CUDA tensor."""
+    if x.dtype != torch.float32 or not x.is_cuda or not x.is_contiguous():
+        raise ValueError("x must be a contiguous fp32 CUDA tensor")
+    if codes is None:
+        codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    st = lib().fp8q_cast_f32(x.data_ptr(), x.numel(), float(scale),
+                             codes.data_ptr(), _stream(x))
+    _check(st, "fp8q_cast_f32")
+    return codes

@@ -1,0 +1,131 @@
+// C-ABI of libfp8q: argument validation, then kernel launches on the
+// caller's stream.  Declarations and contracts are in include/fp8q.h.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fp8q.h"
+#include "internal.h"
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+bool valid_granularity(int g) { return g >= FP8Q_TENSOR && g <= FP8Q_BLOCK_128x128; }
+
+int transposed_granularity(int g) {
+  switch (g) {
+    case FP8Q_ROW: return FP8Q_COL;
+    case FP8Q_COL: return FP8Q_ROW;
+    case FP8Q_BLOCK_1x128: return FP8Q_BLOCK_128x1;
+    case FP8Q_BLOCK_128x1: return FP8Q_BLOCK_1x128;
+    default: return g;
+  }
+}
+
+int64_t count_for(int64_t rows, int64_t cols, int g) {
+  switch (g) {
+    case FP8Q_TENSOR: return 1;
+    case FP8Q_ROW: return rows;
+    case FP8Q_COL: return cols;
+    case FP8Q_BLOCK_1x128: return rows * (cols / 128);
+    case FP8Q_BLOCK_128x1: return (rows / 128) * cols;
+    case FP8Q_BLOCK_128x128: return (rows / 128) * (cols / 128);
+    default: return -1;
+  }
+}
+
+fp8q_status from_hip(hipError_t e) { return e == hipSuccess ? FP8Q_OK : FP8Q_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g, unsigned flags) {
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~FP8Q_OUT_TRANSPOSED)) return -1;
+  const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
+  const int64_t orows = t ? cols : rows, ocols = t ? rows : cols;
+  return count_for(orows, ocols, t ? transposed_granularity(g) : g);
+}
+
+fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx, fp8q_granularity g,
+                          unsigned flags, uint8_t* codes, int64_t ldc, float* scales,
+                          struct ihipStream_t* stream) {
+  if (!x || !codes || !scales) return FP8Q_ERR_INVAL;
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~FP8Q_OUT_TRANSPOSED))
+    return FP8Q_ERR_INVAL;
+  const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
+  if (ldx < cols || ldc < (t ? rows : cols)) return FP8Q_ERR_INVAL;
+  const bool splits_cols = g == FP8Q_BLOCK_1x128 || g == FP8Q_BLOCK_128x128;
+  const bool splits_rows = g == FP8Q_BLOCK_128x1 || g == FP8Q_BLOCK_128x128;
+  if (cols % 16 || (t && rows % 16)) return FP8Q_ERR_UNSUPPORTED;
+  if ((splits_cols && cols % 128) || (splits_rows && rows % 128)) return FP8Q_ERR_UNSUPPORTED;
+  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || ldx % 8 || ldc % 16)
+    return FP8Q_ERR_ALIGN;
+  fp8q::QuantArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.rows = rows;
+  a.cols = cols;
+  a.ldx = ldx;
+  a.codes = codes;
+  a.ldc = ldc;
+  a.scales = scales;
+  const int64_t n = fp8q_scales_count(rows, cols, g, flags);
+  return from_hip(fp8q::launch_quantize(a, g, t, n, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                      const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                      void* C, int64_t ldc, struct ihipStream_t* stream) {
+  if (!A || !sA || !B || !sB || !C) return FP8Q_ERR_INVAL;
+  if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
+  if (lda < K || ldb < K || ldc < N) return FP8Q_ERR_INVAL;
+  int pair;
+  if (gA == FP8Q_TENSOR && gB == FP8Q_TENSOR)
+    pair = fp8q::kPairTensor;
+  else if (gA == FP8Q_ROW && gB == FP8Q_ROW)
+    pair = fp8q::kPairRow;
+  else if (gA == FP8Q_BLOCK_1x128 && gB == FP8Q_BLOCK_128x128)
+    pair = fp8q::kPairBlock;
+  else if (gA == FP8Q_BLOCK_1x128 && gB == FP8Q_BLOCK_1x128)
+    pair = fp8q::kPairBlockK;
+  else
+    return FP8Q_ERR_UNSUPPORTED;
+  if (K % 128 || (gB == FP8Q_BLOCK_128x128 && N % 128)) return FP8Q_ERR_UNSUPPORTED;
+  if (((M + 127) / 128) * ((N + 127) / 128) > 0x7fffffff) return FP8Q_ERR_UNSUPPORTED;
+  if (!aligned(A, 16) || !aligned(B, 16) || lda % 16 || ldb % 16 || !aligned(C, 8) || ldc % 4 ||
+      !aligned(sA, 4) || !aligned(sB, 4))
+    return FP8Q_ERR_ALIGN;
+  fp8q::GemmArgs g;
+  g.A = A;
+  g.B = B;
+  g.sA = sA;
+  g.sB = sB;
+  g.C = static_cast<uint16_t*>(C);
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  return from_hip(fp8q::launch_gemm(g, pair, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, struct ihipStream_t* stream) {
+  if (!x || !codes || n <= 0 || !(scale > 0.0f)) return FP8Q_ERR_INVAL;
+  if (!aligned(x, 4)) return FP8Q_ERR_ALIGN;
+  return from_hip(fp8q::launch_cast_f32(x, n, scale, codes, reinterpret_cast<hipStream_t>(stream)));
+}
+
+const char* fp8q_status_string(fp8q_status s) {
+  switch (s) {
+    case FP8Q_OK: return "FP8Q_OK";
+    case FP8Q_ERR_INVAL: return "FP8Q_ERR_INVAL: invalid argument";
+    case FP8Q_ERR_UNSUPPORTED: return "FP8Q_ERR_UNSUPPORTED: unsupported shape or granularity";
+    case FP8Q_ERR_ALIGN: return "FP8Q_ERR_ALIGN: misaligned pointer or leading dimension";
+    case FP8Q_ERR_HIP: return "FP8Q_ERR_HIP: HIP launch failed";
+    default: return "unknown fp8q status";
+  }
+}
+
+}  // extern "C"

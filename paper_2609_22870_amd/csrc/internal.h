@@ -1,0 +1,35 @@
+// Internal interface between the C-ABI layer and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fp8q {
+
+struct QuantArgs {
+  const uint16_t* x;  // bf16 bit patterns [rows][ldx]
+  int64_t rows, cols, ldx;
+  uint8_t* codes;     // [rows][ldc] or [cols][ldc] when transposed
+  int64_t ldc;
+  float* scales;
+};
+
+// granularity: the fp8q_granularity value; nscales: entries of `scales`.
+hipError_t launch_quantize(const QuantArgs& a, int granularity, bool transposed, int64_t nscales,
+                           hipStream_t s);
+hipError_t launch_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, hipStream_t s);
+
+struct GemmArgs {
+  const uint8_t* A;  // E4M3 [M][lda]
+  const uint8_t* B;  // E4M3 [N][ldb]
+  const float* sA;
+  const float* sB;
+  uint16_t* C;       // bf16 [M][ldc]
+  int64_t M, N, K, lda, ldb, ldc;
+};
+
+enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3 };
+
+hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s);
+
+}  // namespace fp8q

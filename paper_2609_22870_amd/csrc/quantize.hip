@@ -1,0 +1,311 @@
+// FP8 scaled quantization (Eq. 3 of the paper, Sec. 2.2) on gfx950.
+//
+// Every kernel works on 128 x 128 tiles of the bf16 input with 256 threads.
+// Thread t holds rows 8*(t/16) .. 8*(t/16)+7 of the tile and the eight
+// columns 8*(t%16) .. 8*(t%16)+7, read as one 16-byte load per row, so each
+// load instruction of a wave covers four 256-byte row segments.  The sixteen
+// lanes of a DPP row then hold one full 128-element tile row, which makes the
+// 1x128 amax a four-step DPP reduction; 128x1 and 128x128 amaxes add a
+// cross-row shuffle and one LDS exchange between the four waves.
+//
+// Granularities whose units span several tiles (tensor, row, column) run in
+// two passes: an amax pass that max-reduces into the scale array with 32-bit
+// atomics on the fp32 bit patterns (non-negative floats order like their
+// bits), then the cast pass, then a small pass that turns each amax into S.
+#include "device_common.h"
+#include "internal.h"
+
+namespace fp8q {
+
+namespace {
+
+constexpr int kTile = 128;
+constexpr int kThreads = 256;
+
+enum Kind { kBlock1x128, kBlock128x1, kBlock128x128, kPreTensor, kPreRow, kPreCol };
+
+struct Tile {
+  float v[8][8];  // [row i][column j] of this thread's 8 x 8 patch
+};
+
+__device__ __forceinline__ void load_tile(const QuantArgs& a, int64_t r0, int64_t c0, Tile& t) {
+  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int64_t c = c0 + cc * 8;
+  const bool col_ok = c < a.cols;
+  uint4 w[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int64_t r = r0 + rg * 8 + i;
+    w[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (col_ok && r < a.rows) w[i] = *reinterpret_cast<const uint4*>(a.x + r * a.ldx + c);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    t.v[i][0] = bf16_lo(w[i].x);
+    t.v[i][1] = bf16_hi(w[i].x);
+    t.v[i][2] = bf16_lo(w[i].y);
+    t.v[i][3] = bf16_hi(w[i].y);
+    t.v[i][4] = bf16_lo(w[i].z);
+    t.v[i][5] = bf16_hi(w[i].z);
+    t.v[i][6] = bf16_lo(w[i].w);
+    t.v[i][7] = bf16_hi(w[i].w);
+  }
+}
+
+__device__ __forceinline__ float row_partial_max(const Tile& t, int i) {
+  float m = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) m = fmaxf(m, fabsf(t.v[i][j]));
+  return m;
+}
+
+__device__ __forceinline__ float col_partial_max(const Tile& t, int j) {
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(t.v[i][j]));
+  return m;
+}
+
+// Column maxima over the whole 128-row tile: eight per thread (its columns).
+__device__ __forceinline__ void tile_col_max(const Tile& t, float* lds_cols /*[4][128]*/, float out[8]) {
+  const int cc = threadIdx.x & 15, wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    float m = across_rows_max(col_partial_max(t, j));
+    if (lane < 16) lds_cols[wave * kTile + cc * 8 + j] = m;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int col = cc * 8 + j;
+    out[j] = fmaxf(fmaxf(lds_cols[col], lds_cols[kTile + col]),
+                   fmaxf(lds_cols[2 * kTile + col], lds_cols[3 * kTile + col]));
+  }
+}
+
+__device__ __forceinline__ float tile_max(const Tile& t, float* lds4) {
+  float m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) m = fmaxf(m, row_partial_max(t, i));
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = m;
+  __syncthreads();
+  return fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3]));
+}
+
+template <int K, bool TRANS>
+__global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
+  __shared__ float lds_red[4 * kTile];
+  __shared__ uint64_t lds_t[TRANS ? kTile * kTile / 8 : 1];
+
+  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int64_t r0 = (int64_t)blockIdx.y * kTile;
+  const int64_t c0 = (int64_t)blockIdx.x * kTile;
+  const int64_t c = c0 + cc * 8;
+
+  Tile t;
+  load_tile(a, r0, c0, t);
+
+  // Per-unit scales for this thread's elements: by row (1x128, ROW),
+  // by column (128x1, COL), or one per tile (128x128, TENSOR).
+  UnitScale us[8];
+  if (K == kBlock1x128) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) us[i] = unit_scale(row16_max(row_partial_max(t, i)));
+  } else if (K == kBlock128x1) {
+    float m[8];
+    tile_col_max(t, lds_red, m);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) us[j] = unit_scale(m[j]);
+  } else if (K == kBlock128x128) {
+    us[0] = unit_scale(tile_max(t, lds_red));
+  } else if (K == kPreTensor) {
+    us[0] = unit_scale(a.scales[0]);
+  } else if (K == kPreRow) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t r = r0 + rg * 8 + i;
+      us[i] = unit_scale(r < a.rows ? a.scales[r] : 0.0f);
+    }
+  } else {  // kPreCol
+#pragma unroll
+    for (int j = 0; j < 8; ++j) us[j] = unit_scale(c + j < a.cols ? a.scales[c + j] : 0.0f);
+  }
+
+  constexpr bool by_row = K == kBlock1x128 || K == kPreRow;
+  constexpr bool by_col = K == kBlock128x1 || K == kPreCol;
+
+  // codes, two E4M3 bytes per conversion; q[i][j] -> byte j of row i
+  uint32_t packed[8][2];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      float q[4];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int j = h * 4 + jj;
+        const UnitScale& u = by_row ? us[i] : (by_col ? us[j] : us[0]);
+        q[jj] = quotient(t.v[i][j], u);
+      }
+      uint32_t w = e4m3_pack2<false>(q[0], q[1], 0u);
+      packed[i][h] = e4m3_pack2<true>(q[2], q[3], w);
+    }
+  }
+
+  if (!TRANS) {
+    if (c < a.cols) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int64_t r = r0 + rg * 8 + i;
+        if (r < a.rows)
+          *reinterpret_cast<uint2*>(a.codes + r * a.ldc + c) = make_uint2(packed[i][0], packed[i][1]);
+      }
+    }
+  } else {
+    // Transpose through LDS: LDS row = tile column (128 bytes = 16 chunks of
+    // 8 rows); chunk rg of LDS row 8*cc+j is stored at chunk rg ^ cc, which
+    // spreads the 16 lanes of a DPP row over all 32 banks.
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      uint32_t lo = 0, hi = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) lo |= ((packed[i][j >> 2] >> (8 * (j & 3))) & 0xffu) << (8 * i);
+#pragma unroll
+      for (int i = 4; i < 8; ++i) hi |= ((packed[i][j >> 2] >> (8 * (j & 3))) & 0xffu) << (8 * (i - 4));
+      const int lrow = cc * 8 + j;
+      lds_t[lrow * 16 + (rg ^ cc)] = (uint64_t)lo | ((uint64_t)hi << 32);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int orow = p * 32 + (threadIdx.x >> 3);  // tile column = output row
+      const int qd = threadIdx.x & 7;                // 16-byte chunk of the output row
+      const int sw = orow >> 3;
+      const uint64_t a0 = lds_t[orow * 16 + ((2 * qd) ^ sw)];
+      const uint64_t a1 = lds_t[orow * 16 + ((2 * qd + 1) ^ sw)];
+      const int64_t oc = c0 + orow;
+      const int64_t orr = r0 + qd * 16;
+      if (oc < a.cols && orr < a.rows)
+        *reinterpret_cast<uint4*>(a.codes + oc * a.ldc + orr) =
+            make_uint4((uint32_t)a0, (uint32_t)(a0 >> 32), (uint32_t)a1, (uint32_t)(a1 >> 32));
+    }
+  }
+
+  // scales of the block granularities (TENSOR / ROW / COL are finalized later)
+  if (K == kBlock1x128) {
+    // output index (c0 / 128) * rows + r, the same for the transposed layout
+    if (cc < 8) {
+      float s = us[0].s;
+#pragma unroll
+      for (int i = 1; i < 8; ++i) s = (cc == i) ? us[i].s : s;
+      const int64_t r = r0 + rg * 8 + cc;
+      if (r < a.rows) a.scales[(int64_t)blockIdx.x * a.rows + r] = s;
+    }
+  } else if (K == kBlock128x1) {
+    // output index (r0 / 128) * cols + c, the same for the transposed layout
+    if (rg == 0 && c < a.cols) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) a.scales[(int64_t)blockIdx.y * a.cols + c + j] = us[j].s;
+    }
+  } else if (K == kBlock128x128) {
+    if (threadIdx.x == 0) {
+      const int64_t idx = TRANS ? (int64_t)blockIdx.x * gridDim.y + blockIdx.y
+                                : (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+      a.scales[idx] = us[0].s;
+    }
+  }
+}
+
+// Amax pass of the two-pass granularities: atomic max of |x| into `scales`
+// (zeroed beforehand) per tensor, row or column.
+template <int K>
+__global__ __launch_bounds__(kThreads) void amax_tile_kernel(QuantArgs a) {
+  __shared__ float lds_red[4 * kTile];
+  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int64_t r0 = (int64_t)blockIdx.y * kTile;
+  const int64_t c0 = (int64_t)blockIdx.x * kTile;
+  Tile t;
+  load_tile(a, r0, c0, t);
+  unsigned int* bits = reinterpret_cast<unsigned int*>(a.scales);
+  if (K == kPreRow) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float m = row16_max(row_partial_max(t, i));
+      const int64_t r = r0 + rg * 8 + i;
+      if (cc == 0 && r < a.rows) atomicMax(bits + r, __float_as_uint(m));
+    }
+  } else if (K == kPreCol) {
+    float m[8];
+    tile_col_max(t, lds_red, m);
+    const int64_t c = c0 + cc * 8;
+    if (rg == 0 && c < a.cols) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) atomicMax(bits + c + j, __float_as_uint(m[j]));
+    }
+  } else {
+    const float m = tile_max(t, lds_red);
+    if (threadIdx.x == 0) atomicMax(bits, __float_as_uint(m));
+  }
+}
+
+__global__ void fill_zero_kernel(float* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0.0f;
+}
+
+__global__ void amax_to_scale_kernel(float* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = unit_scale(p[i]).s;
+}
+
+__global__ void cast_f32_kernel(const float* x, int64_t n, float scale, uint8_t* codes) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+    const float q = x[i] / scale;  // IEEE division: any fp32 x and scale
+    codes[i] = (uint8_t)(e4m3_pack2<false>(q, q, 0u) & 0xffu);
+  }
+}
+
+template <int K, bool TRANS>
+hipError_t launch_tile(const QuantArgs& a, hipStream_t s) {
+  const dim3 grid((unsigned)((a.cols + kTile - 1) / kTile), (unsigned)((a.rows + kTile - 1) / kTile));
+  quant_tile_kernel<K, TRANS><<<grid, kThreads, 0, s>>>(a);
+  return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipStream_t s) {
+  const unsigned fill_blocks = (unsigned)((nscales + 255) / 256 < 4096 ? (nscales + 255) / 256 : 4096);
+  fill_zero_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 grid((unsigned)((a.cols + kTile - 1) / kTile), (unsigned)((a.rows + kTile - 1) / kTile));
+  amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  e = trans ? launch_tile<K, true>(a, s) : launch_tile<K, false>(a, s);
+  if (e != hipSuccess) return e;
+  amax_to_scale_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const QuantArgs& a, int granularity, bool trans, int64_t nscales, hipStream_t s) {
+  switch (granularity) {
+    case 3: return trans ? launch_tile<kBlock1x128, true>(a, s) : launch_tile<kBlock1x128, false>(a, s);
+    case 4: return trans ? launch_tile<kBlock128x1, true>(a, s) : launch_tile<kBlock128x1, false>(a, s);
+    case 5: return trans ? launch_tile<kBlock128x128, true>(a, s) : launch_tile<kBlock128x128, false>(a, s);
+    case 0: return launch_two_pass<kPreTensor>(a, trans, nscales, s);
+    case 1: return launch_two_pass<kPreRow>(a, trans, nscales, s);
+    case 2: return launch_two_pass<kPreCol>(a, trans, nscales, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, hipStream_t s) {
+  const int64_t blocks = (n + 255) / 256;
+  cast_f32_kernel<<<(unsigned)(blocks < 8192 ? blocks : 8192), 256, 0, s>>>(x, n, scale, codes);
+  return hipGetLastError();
+}
+
+}  // namespace fp8q

@@ -1,0 +1,132 @@
+"""The C-ABI library loads without a GPU, exports every entry point that
+include/fp8q.h declares, and rejects bad arguments on the host before any
+HIP call (so no GPU is touched here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fp8q.h")
+
+fp8q = pytest.importorskip("paper_2609_22870_amd")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(fp8q.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return fp8q.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fp8q_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_abi():
+    assert declared_functions() == sorted(fp8q.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    out = os.popen("nm -D --defined-only %s" % fp8q.LIB_PATH).read()
+    for name in declared_functions():
+        assert re.search(r"\bT %s\b" % name, out), name
+
+
+def test_status_strings(L):
+    for s in (0, -1, -2, -3, -4):
+        assert fp8q.status_string(s).startswith("FP8Q_")
+
+
+@pytest.mark.parametrize("rows,cols,g,t,want", [
+    (256, 384, fp8q.TENSOR, False, 1),
+    (256, 384, fp8q.ROW, False, 256),
+    (256, 384, fp8q.ROW, True, 256),
+    (256, 384, fp8q.COL, False, 384),
+    (256, 384, fp8q.BLOCK_1x128, False, 256 * 3),
+    (256, 384, fp8q.BLOCK_1x128, True, 256 * 3),
+    (256, 384, fp8q.BLOCK_128x1, False, 2 * 384),
+    (256, 384, fp8q.BLOCK_128x1, True, 2 * 384),
+    (256, 384, fp8q.BLOCK_128x128, False, 6),
+    (256, 384, fp8q.BLOCK_128x128, True, 6),
+    (0, 384, fp8q.TENSOR, False, -1),
+    (256, 384, 9, False, -1),
+])
+def test_scales_count(L, rows, cols, g, t, want):
+    assert L.fp8q_scales_count(rows, cols, g, 1 if t else 0) == want
+
+
+FAKE = 0x10000  # never dereferenced: every case below fails validation
+
+
+def quant(L, x=FAKE, rows=256, cols=256, ldx=256, g=3, flags=0, codes=FAKE,
+          ldc=256, scales=FAKE):
+    return L.fp8q_quantize(x, rows, cols, ldx, g, flags, codes, ldc, scales, None)
+
+
+def test_quantize_rejections(L):
+    assert quant(L, x=None) == -1
+    assert quant(L, codes=None) == -1
+    assert quant(L, scales=None) == -1
+    assert quant(L, rows=0) == -1
+    assert quant(L, cols=-5) == -1
+    assert quant(L, g=6) == -1
+    assert quant(L, flags=2) == -1
+    assert quant(L, ldx=128) == -1
+    assert quant(L, ldc=128) == -1
+    assert quant(L, cols=200, ldx=200, ldc=208) == -2        # cols % 16
+    assert quant(L, cols=272, ldx=272, ldc=272) == -2        # 1x128 needs cols % 128
+    assert quant(L, rows=200, g=4) == -2                     # 128x1 needs rows % 128
+    assert quant(L, rows=200, g=5) == -2
+    assert quant(L, rows=200, g=1, flags=1, ldc=208) == -2   # transposed: rows % 16
+    assert quant(L, x=FAKE + 2) == -3
+    assert quant(L, codes=FAKE + 8) == -3
+    assert quant(L, scales=FAKE + 2) == -3
+    assert quant(L, ldx=260) == -3
+    assert quant(L, ldc=264) == -3
+
+
+def gemm(L, A=FAKE, sA=FAKE, gA=3, lda=256, B=FAKE, sB=FAKE, gB=5, ldb=256,
+         M=256, N=256, K=256, C=FAKE, ldc=256):
+    return L.fp8q_gemm(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, C, ldc, None)
+
+
+def test_gemm_rejections(L):
+    assert gemm(L, A=None) == -1
+    assert gemm(L, sB=None) == -1
+    assert gemm(L, C=None) == -1
+    assert gemm(L, M=0) == -1
+    assert gemm(L, lda=128) == -1
+    assert gemm(L, ldc=100) == -1
+    assert gemm(L, gA=7) == -1
+    assert gemm(L, gA=0, gB=1) == -2
+    assert gemm(L, gA=5, gB=5) == -2
+    assert gemm(L, gA=3, gB=4) == -2
+    assert gemm(L, K=200, lda=256, ldb=256) == -2
+    assert gemm(L, N=200, ldc=256) == -2                     # 128x128 B needs N % 128
+    assert gemm(L, A=FAKE + 4) == -3
+    assert gemm(L, lda=264) == -3
+    assert gemm(L, C=FAKE + 2) == -3
+    assert gemm(L, ldc=258) == -3
+
+
+def test_cast_rejections(L):
+    assert L.fp8q_cast_f32(None, 10, 1.0, FAKE, None) == -1
+    assert L.fp8q_cast_f32(FAKE, 0, 1.0, FAKE, None) == -1
+    assert L.fp8q_cast_f32(FAKE, 10, 0.0, FAKE, None) == -1
+    assert L.fp8q_cast_f32(FAKE, 10, -1.0, FAKE, None) == -1
+    assert L.fp8q_cast_f32(FAKE + 1, 10, 1.0, FAKE, None) == -3
+
+
+def test_no_cpu_fallback_when_library_missing(monkeypatch, tmp_path):
+    """Without the built library the binding raises instead of computing."""
+    monkeypatch.setattr(fp8q, "LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(fp8q, "_lib", None)
+    with pytest.raises(ImportError):
+        fp8q.lib()

@@ -1,0 +1,190 @@
+"""GPU parity of the quantizer (Eq. 3, paper Sec. 2.2) against the oracle:
+codes and scales must match bit for bit.  Calls go through the C-ABI."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_22870_amd as fp8q
+from paper_2609_22870_amd import synth
+
+import _par
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+G_ALL = [fp8q.TENSOR, fp8q.ROW, fp8q.COL, fp8q.BLOCK_1x128, fp8q.BLOCK_128x1,
+         fp8q.BLOCK_128x128]
+
+
+def check(x, g, transposed=False, label=""):
+    """Quantize x (bf16 CPU tensor) on the GPU and with the oracle."""
+    print("quantize parity", label, tuple(x.shape), "g=%d t=%d" % (g, transposed), flush=True)
+    codes, scales = fp8q.quantize(x.to(DEV), g, transposed)
+    torch.cuda.synchronize()
+    oc, os_ = _par.quantize(synth.bf16_bits(x), g, transposed)
+    gc, gs = codes.cpu().numpy(), scales.cpu().numpy()
+    assert gs.shape == os_.shape
+    bad_s = np.nonzero(gs.view(np.uint32) != os_.view(np.uint32))[0]
+    assert bad_s.size == 0, "scales differ at %s: %r vs %r" % (bad_s[:5], gs[bad_s[:5]], os_[bad_s[:5]])
+    bad = np.argwhere(gc != oc)
+    assert bad.size == 0, "codes differ at %s" % bad[:5]
+
+
+@pytest.mark.parametrize("g", G_ALL)
+@pytest.mark.parametrize("transposed", [False, True])
+def test_small_all_granularities(g, transposed):
+    # several tiles in both directions and, where the granularity allows,
+    # a ragged last tile of rows (272 = 2 * 128 + 16) and of columns
+    rows = 256 if g in (fp8q.BLOCK_128x1, fp8q.BLOCK_128x128) else 272
+    cols = 384 if g in (fp8q.BLOCK_1x128, fp8q.BLOCK_128x128) else 400
+    x = synth.activations(rows, cols, seed=11 + g, outlier_seed=12 + g)
+    check(x, g, transposed, "small")
+
+
+@pytest.mark.parametrize("g", [fp8q.ROW, fp8q.TENSOR, fp8q.BLOCK_1x128])
+def test_single_row_and_narrow(g):
+    cols = 128
+    check(synth.activations(1, cols, seed=3, outlier_seed=4), g, label="one row")
+    check(synth.activations(48, 16 if g != fp8q.BLOCK_1x128 else 128, seed=5, outlier_seed=6), g,
+          label="narrow")
+
+
+def test_padded_leading_dimensions():
+    x = synth.activations(200, 512, seed=21, outlier_seed=22)
+    xd = torch.zeros((200, 640), dtype=torch.bfloat16, device=DEV)
+    xd[:, :512] = x.to(DEV)
+    view = xd[:, :512]
+    codes = torch.full((200, 528), 0x5A, dtype=torch.uint8, device=DEV)
+    cview = codes[:, :512]
+    scales = torch.empty(fp8q.scales_count(200, 512, fp8q.BLOCK_1x128), dtype=torch.float32, device=DEV)
+    fp8q.quantize(view, fp8q.BLOCK_1x128, codes=cview, scales=scales)
+    oc, os_ = oracle.quantize(synth.bf16_bits(x), oracle.BLOCK_1x128)
+    assert np.array_equal(cview.cpu().numpy(), oc)
+    assert np.array_equal(scales.cpu().numpy(), os_)
+    assert torch.all(codes[:, 512:] == 0x5A)  # padding untouched
+
+
+def test_special_blocks():
+    """All-zero, signed-zero, single-nonzero, constant-magnitude and
+    subnormal-amax blocks, each a 1x128 block of one row."""
+    rows = []
+    rows.append([0.0] * 128)
+    rows.append([-0.0] * 64 + [0.0] * 64)
+    r = [0.0] * 128
+    r[9] = -3.25
+    rows.append(r)
+    rows.append([0.75 if i % 3 else -0.75 for i in range(128)])
+    rows.append([2.0 ** -133 * (i % 5) for i in range(127)] + [-(2.0 ** -128)])
+    rows.append([2.0 ** -140 * (i % 3) for i in range(128)])
+    rows.append([3.0e38 if i == 0 else -1.0e38 * (i % 2) for i in range(128)])
+    t = torch.tensor(rows, dtype=torch.float32).to(torch.bfloat16)
+    t = torch.cat([t] * 16, 0)  # 112 rows
+    for g in (fp8q.BLOCK_1x128, fp8q.ROW, fp8q.TENSOR, fp8q.BLOCK_128x1 if t.shape[0] % 128 == 0 else fp8q.COL):
+        check(t, g, label="special")
+        check(t, g, transposed=True, label="special")
+
+
+def test_guard_bands_and_determinism():
+    x = synth.activations(384, 512, seed=31, outlier_seed=32).to(DEV)
+    n = 384 * 512
+    buf = torch.full((n + 4096,), 0xA5, dtype=torch.uint8, device=DEV)
+    codes = buf[2048:2048 + n].view(384, 512)
+    ns = fp8q.scales_count(384, 512, fp8q.BLOCK_1x128)
+    sbuf = torch.full((ns + 64,), -7.0, dtype=torch.float32, device=DEV)
+    scales = sbuf[32:32 + ns]
+    fp8q.quantize(x, fp8q.BLOCK_1x128, codes=codes, scales=scales)
+    first = (codes.clone(), scales.clone())
+    fp8q.quantize(x, fp8q.BLOCK_1x128, codes=codes, scales=scales)
+    torch.cuda.synchronize()
+    assert torch.all(buf[:2048] == 0xA5) and torch.all(buf[2048 + n:] == 0xA5)
+    assert torch.all(sbuf[:32] == -7.0) and torch.all(sbuf[32 + ns:] == -7.0)
+    assert torch.equal(first[0], codes) and torch.equal(first[1], scales)
+
+
+def all_bf16_pairs(device):
+    """Rows of 128 bf16: element 0 is an amax a, the others walk through every
+    bf16 magnitude from 0 up to a (signs from a fixed hash of the position);
+    every positive finite bf16 a is covered, so every (amax, x) pair of the
+    1x128 path occurs."""
+    a = torch.arange(1, 0x7F80, dtype=torch.int64, device=device)  # positive finite bf16
+    per = (a + 1 + 126) // 127                                      # rows per amax
+    row_a = torch.repeat_interleave(a, per)
+    starts = torch.repeat_interleave(torch.cumsum(per, 0) - per, per)
+    first = torch.arange(row_a.numel(), dtype=torch.int64, device=device) - starts
+    j = torch.arange(127, dtype=torch.int64, device=device)[None, :]
+    xb = first[:, None] * 127 + j                                   # magnitudes 0 .. a
+    xb = torch.where(xb <= row_a[:, None], xb, torch.zeros_like(xb))
+    pos = torch.arange(xb.numel(), dtype=torch.int64, device=device).view(xb.shape)
+    sign = ((pos * 0x9E3779B1) >> 17) & 0x8000
+    out = torch.cat([row_a[:, None], xb | sign], 1).to(torch.int32)
+    return out.to(torch.int16).view(torch.bfloat16)
+
+
+def test_exhaustive_bf16_amax_x_pairs():
+    x = all_bf16_pairs(DEV)
+    print("exhaustive pairs: rows", x.shape[0], flush=True)
+    codes, scales = fp8q.quantize(x, fp8q.BLOCK_1x128)
+    torch.cuda.synchronize()
+    gc, gs = codes.cpu().numpy(), scales.cpu().numpy()
+    bits = synth.bf16_bits(x)
+    del codes, scales, x
+    # coverage of the construction itself
+    mag = bits[:, 1:] & 0x7FFF
+    assert np.all(mag <= bits[:, :1]) and np.unique(bits[:, 0]).size == 0x7F7F
+    oc, os_ = _par.quantize(bits, oracle.BLOCK_1x128)
+    assert np.array_equal(gs.view(np.uint32), os_.view(np.uint32))
+    assert np.array_equal(gc, oc)
+
+
+def test_cast_f32_all_patterns():
+    """The device rounding routine on all 2^32 fp32 patterns (scale 1),
+    NaN inputs excluded, in 2^28-pattern chunks."""
+    chunk = 1 << 28
+    for start in range(0, 1 << 32, chunk):
+        print("cast sweep chunk", hex(start), flush=True)
+        bits = np.arange(start, start + chunk, dtype=np.uint64).astype(np.uint32)
+        x = torch.from_numpy(bits.view(np.int32)).view(torch.float32)
+        got = fp8q.cast_f32(x.to(DEV), 1.0).cpu().numpy()
+        vals = bits.view(np.float32)
+        keep = ~np.isnan(vals)
+        want = _par.cast_f32(vals, 1.0)
+        assert np.array_equal(got[keep], want[keep]), hex(start)
+
+
+@pytest.mark.parametrize("scale", [0.37, 3.0e-5, 1.7e30])
+def test_cast_f32_scaled(scale):
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal(1 << 20) * 448 * scale).astype(np.float32)
+    got = fp8q.cast_f32(torch.from_numpy(x).to(DEV), scale).cpu().numpy()
+    assert np.array_equal(got, oracle.cast_f32(x, scale))
+
+
+# ---- the quantized operands of the named workloads, full size
+
+def test_full_8b_forward_operands():
+    """8B-class FFN up-projection: X 16384 x 4096 (1x128), W 12288 x 4096
+    (128x128, plain for forward and transposed for dgrad)."""
+    x = synth.activations(16384, 4096, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=DEV)
+    check(x.cpu(), fp8q.BLOCK_1x128, label="X 8B")
+    w = synth.weights(12288, 4096, seed=synth.seed_for(2, 1), device=DEV)
+    check(w.cpu(), fp8q.BLOCK_128x128, label="W 8B")
+    check(w.cpu(), fp8q.BLOCK_128x128, transposed=True, label="W^T 8B")
+
+
+def test_full_8b_rowwise_operands():
+    x = synth.activations(16384, 4096, seed=synth.seed_for(3, 0), outlier_seed=synth.seed_for(3, 3), device=DEV)
+    check(x.cpu(), fp8q.ROW, label="X rowwise")
+    w = synth.weights(12288, 4096, seed=synth.seed_for(3, 1), device=DEV)
+    check(w.cpu(), fp8q.ROW, label="W rowwise")
+
+
+def test_full_32b_backward_operands():
+    """32B-class: dY 16384 x 25600 ~ N(0, 1e-3), 1x128 for dgrad and 128x1
+    transposed for wgrad; X 16384 x 5120 128x1 transposed for wgrad."""
+    dy = synth.grads(16384, 25600, seed=synth.seed_for(5, 2), device=DEV).cpu()
+    check(dy, fp8q.BLOCK_1x128, label="dY 32B")
+    check(dy, fp8q.BLOCK_128x1, transposed=True, label="dY^T 32B")
+    del dy
+    x = synth.activations(16384, 5120, seed=synth.seed_for(5, 0), outlier_seed=synth.seed_for(5, 3), device=DEV)
+    check(x.cpu(), fp8q.BLOCK_128x1, transposed=True, label="X^T 32B")
