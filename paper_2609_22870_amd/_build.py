@@ -40,6 +40,12 @@ def build():
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s" % r.stderr)
+    # every symbol must resolve (a missing kernel stub only shows at load)
+    r = subprocess.run(["python3", "-c", "import ctypes, sys; ctypes.CDLL(sys.argv[1])", tmp],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        os.unlink(tmp)
+        raise RuntimeError("built library does not load:\n%s" % r.stderr)
     os.replace(tmp, LIB)
     return LIB
 

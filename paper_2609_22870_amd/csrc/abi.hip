@@ -108,6 +108,11 @@ fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, in
   g.lda = lda;
   g.ldb = ldb;
   g.ldc = ldc;
+  g.sa_ld = M;
+  g.sb_ld = N;
+  g.sa_count = count_for(M, K, gA);
+  g.sb_count = count_for(N, K, gB);
+  g.c_aligned16 = aligned(C, 16) && ldc % 8 == 0;
   return from_hip(fp8q::launch_gemm(g, pair, reinterpret_cast<hipStream_t>(stream)));
 }
 

@@ -8,10 +8,9 @@
 // of one scale block, so a blockwise step is one MFMA per 16 x 16 tile into
 // a zeroed partial, then one FMA per accumulator that adds S_A * S_B * P.
 //
-// Operand tiles (128 rows x 128 bytes of K) go global -> LDS with the
-// direct-to-LDS 16-byte loads of gfx950 (no VGPR staging), double buffered.
-// In LDS the 16-byte chunk c of row r is stored at chunk c ^ (r & 7), so the
-// eight rows read together by a ds_read_b128 hit eight different chunks.
+// Operand tiles (rows x 128 bytes of K) go global -> LDS with the
+// direct-to-LDS 16-byte buffer loads of gfx950 (no VGPR staging), double
+// buffered, XOR-swizzled against LDS bank conflicts.
 // The MFMA "A" operand is the B tile (rows n) and the MFMA "B" operand the A
 // tile (rows m): each lane then ends with four consecutive n of one m, which
 // the epilogue stores as one 8-byte bf16x4.
@@ -20,16 +19,13 @@
 
 namespace fp8q {
 
-namespace {
+namespace gemm_detail {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 128;
-constexpr int kThreads = 256;
-constexpr int kTileBytes = kBM * kBK;        // one operand tile, 16 KB
-constexpr int kStageBytes = 2 * kTileBytes;  // A tile + B tile
-constexpr int kGroupM = 8;                   // tile rows per group of the raster
+constexpr int kBK = 128;
+constexpr int kGroupM = 8;  // tile rows per group of the raster
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -44,46 +40,168 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return u >> 16;
 }
 
-// Copy one 128 x 128-byte operand tile (rows row0.., K bytes k0..) into LDS.
-// Each wave moves four groups of eight rows; lane l of a group lands at byte
-// 16 * l of the group's 1 KB, i.e. row l / 8, physical chunk l % 8, so it
-// fetches logical chunk (l % 8) ^ (l / 8).  Rows past `rows` are clamped to
-// the last row (their results are never stored).
-__device__ __forceinline__ void load_tile_lds(const uint8_t* base, int64_t ld, int64_t row0, int64_t rows,
-                                              int64_t k0, uint8_t* lds_tile) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int chunk = (lane & 7) ^ (lane >> 3);
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const int grp = wave * 4 + g;  // 16 groups of 8 rows
-    int64_t r = row0 + grp * 8 + (lane >> 3);
-    r = r < rows ? r : rows - 1;
-    const uint8_t* src = base + r * ld + k0 + chunk * 16;
-    __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)(lds_tile + grp * 1024), 16, 0, 0);
-  }
+// Buffer resource over `bytes` bytes at `base` (gfx9 raw buffer: stride 0,
+// loads past `bytes` return zero, stores past it are dropped).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// 32 K-bytes of one operand row for the MFMA: logical chunks 2g and 2g+1
-// of row `row` (g = lane / 16), un-swizzled.
-__device__ __forceinline__ v8i read_frag(const uint8_t* lds_tile, int row) {
+__device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
+// Copies of ROWS x 128-byte operand tiles (K bytes k0 .. k0+127) into LDS
+// with direct buffer-to-LDS loads.  In LDS the 16-byte chunk c of tile row r
+// sits at chunk c ^ ((r >> 1) & 7): the LDS has 64 banks (256 bytes), a
+// ds_read_b128 serves 16 lanes at a time, and the 16 rows read together
+// (two per 256 bytes) then hit 16 different 16-byte slots.  A wave
+// instruction moves a group of eight rows: lane l lands at byte 16 l of the
+// group's 1 KB, i.e. row l / 8, physical chunk l % 8, so it fetches the
+// logical chunk that maps there.  Each
+// lane keeps one 32-bit row offset per group; rows past the operand read as
+// zero through the buffer bounds (their results are never stored).
+template <int ROWS, int NWAVES>
+struct TileLoader {
+  static constexpr int kGroups = ROWS / 8;
+  static constexpr int kPerWave = kGroups / NWAVES;
+  static_assert(kGroups % NWAVES == 0, "row groups must split evenly over the waves");
+  static_assert(kPerWave % 2 == 0, "groups come in pairs (the swizzle repeats every 16 rows)");
+  __amdgpu_buffer_rsrc_t rsrc;
+  int off_even, off_odd;  // this lane's offset for the wave's first group, and the second
+  int step;               // byte distance between groups g and g+2 (16 rows)
+
+  __device__ __forceinline__ TileLoader(const uint8_t* base, int64_t ld, int64_t row0, int64_t rows, int wave) {
+    rsrc = make_rsrc(base, (uint32_t)(rows * ld));
+    const int lane = threadIdx.x & 63;
+    const int trow = wave * kPerWave * 8 + (lane >> 3);  // tile row of group 0 (kPerWave even)
+    // the chunk swizzle depends on (trow >> 1) & 7, which differs between
+    // even and odd groups only
+    const int chunk_even = (lane & 7) ^ ((trow >> 1) & 7);
+    const int chunk_odd = (lane & 7) ^ (((trow + 8) >> 1) & 7);
+    const int64_t r = row0 + trow;
+    // rows past the operand give offsets past the buffer: they read zero
+    off_even = (int)(r * ld) + chunk_even * 16;
+    off_odd = (int)((r + 8) * ld) + chunk_odd * 16;
+    step = (int)(16 * ld);
+  }
+
+  __device__ __forceinline__ void load(int k0, uint8_t* lds_tile, int wave) const {
+#pragma unroll
+    for (int g = 0; g < kPerWave; ++g) {
+      const int off = (g & 1 ? off_odd : off_even) + (g >> 1) * step;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_tile + (wave * kPerWave + g) * 1024), 16,
+                                               off, k0, 0, 0);
+    }
+  }
+};
+
+// Touches every 128-byte line of one K block of the A and B tiles with a
+// 4-byte direct-to-LDS load into a scratch corner of LDS: the lines are
+// pulled into L2 one K step before the tile loads fetch them, which then hit
+// L2 instead of waiting on memory.  No VGPR is involved, so the loads can
+// stay outstanding across a step.
+template <int BM, int BN, int NWAVES>
+struct LinePrefetcher {
+  static constexpr int kLines = BM + BN;
+  static_assert(kLines == NWAVES * 64, "one line per lane");
+  __amdgpu_buffer_rsrc_t rsrc;
+  int off;
+
+  __device__ __forceinline__ LinePrefetcher(const uint8_t* A, int64_t lda, int64_t m0, int64_t M,
+                                            const uint8_t* B, int64_t ldb, int64_t n0, int64_t N,
+                                            bool is_b) {
+    const int t = threadIdx.x;
+    const int64_t r = is_b ? n0 + (t - BM) : m0 + t;
+    const int64_t rows = is_b ? N : M, ld = is_b ? ldb : lda;
+    rsrc = make_rsrc(is_b ? B : A, (uint32_t)(rows * ld));
+    off = r < rows ? (int)(r * ld) : (int)0x7fffffff;
+  }
+
+  __device__ __forceinline__ void touch(int k0, uint8_t* scratch, int wave) const {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(scratch + wave * 256), 4, off, k0, 0, 0);
+  }
+};
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+__device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
+  return (uint32_t)(uintptr_t)(const lds_u8*)p;
+}
+
+// Issue the reads of 32 K-bytes of one operand row for the MFMA: logical
+// chunks 2g and 2g+1 of tile row `row` (g = lane / 16), un-swizzled.  The
+// reads are inline asm: the compiler then sees no LDS load it would have to
+// order after the direct-to-LDS loads still in flight for the next stage (it
+// would otherwise wait for all of them before every step).  The data is
+// ready only after a later lds_wait naming the fragment.
+//
+// Because the compiler does not see these as register writes, two rules
+// keep them clear of matrix instructions that may still be reading their
+// sources: the destination is early-clobber against `busy` and `busy2`,
+// fragments of MFMAs possibly in flight or still to be issued (so it never
+// takes those registers), and the
+// address depends on `after`, a VALU result computed from the output of the
+// last MFMA whose source registers may be reused (so that MFMA is done).
+__device__ __forceinline__ v8i read_frag(const uint8_t* lds_tile, int row, const v8i& busy, const v8i& busy2,
+                                         float after) {
   const int g = (threadIdx.x & 63) >> 4;
-  const int sw = row & 7;
-  const uint4 lo = *reinterpret_cast<const uint4*>(lds_tile + row * 128 + (((2 * g) ^ sw) << 4));
-  const uint4 hi = *reinterpret_cast<const uint4*>(lds_tile + row * 128 + (((2 * g + 1) ^ sw) << 4));
+  const int sw = (row >> 1) & 7;
+  uint32_t base = lds_addr(lds_tile) + row * 128;
+  asm volatile("" : "+v"(base) : "v"(after));
+  const uint32_t a_lo = base + (((2 * g) ^ sw) << 4);
+  const uint32_t a_hi = base + (((2 * g + 1) ^ sw) << 4);
+  uint4 lo, hi;
+  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3"
+               : "=&v"(lo), "=&v"(hi)
+               : "v"(a_lo), "v"(a_hi), "v"(busy), "v"(busy2));
   v8i f;
   f[0] = (int)lo.x; f[1] = (int)lo.y; f[2] = (int)lo.z; f[3] = (int)lo.w;
   f[4] = (int)hi.x; f[5] = (int)hi.y; f[6] = (int)hi.z; f[7] = (int)hi.w;
   return f;
 }
 
+// Scalar and 4-wide fp32 reads from LDS, completed by the next lds_wait
+// (the values may only be used after it).
+__device__ __forceinline__ float lds_read_f32(uint32_t addr, int imm) {
+  float v;
+  asm volatile("ds_read_b32 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(imm));
+  return v;
+}
+__device__ __forceinline__ void lds_read_f32x4(uint32_t addr, float (&v)[4]) {
+  float4 t;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(t) : "v"(addr));
+  v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+}
+
+// Wait until at most N LDS reads of this wave are outstanding, and make
+// `f` (whose reads were issued before the last N) count as written here.
+// The loop issues no scalar memory loads, so LDS reads retire in order.
+template <int N>
+__device__ __forceinline__ void lds_wait(v8i& f) {
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(f) : "n"(N));
+}
+
 __device__ __forceinline__ void wait_vmem_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// all but the last vector-memory instruction of this wave have completed
+__device__ __forceinline__ void wait_vmem_but_one() { asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); }
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Empty asm that claims to read `done` and rewrite `next`: whatever consumes
+// `next` afterwards is ordered after everything that produced `done`.
+template <int TJ>
+__device__ __forceinline__ void order_after(v8i& next, v4f (&done)[TJ]) {
+  asm volatile("" : "+v"(next) : "v"(done[0]), "v"(done[TJ - 1]));
+  if (TJ > 2) asm volatile("" : "+v"(next) : "v"(done[1]), "v"(done[TJ > 2 ? 2 : 0]));
+}
 
 // Tile coordinates of this workgroup.  Workgroup b runs on XCD b % 8, so
 // each XCD is given a contiguous range of the raster (sharing its L2), and
 // the raster walks kGroupM tile rows at a time so that consecutive tiles
 // reuse A rows and B rows.
+template <int BM, int BN>
 __device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int& tm, int& tn) {
-  const int tiles_m = (int)((M + kBM - 1) / kBM), tiles_n = (int)((N + kBN - 1) / kBN);
+  const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
   const int total = tiles_m * tiles_n;
   const int b = blockIdx.x;
   const int xcd = b & 7, per = total >> 3, extra = total & 7;
@@ -97,159 +215,352 @@ __device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int& tm, int& 
   tn = in_group / gsize;
 }
 
-template <int PAIR>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStageBytes];
+// One workgroup computes a BM x BN tile of C with (BM/WM) x (BN/WN) waves,
+// each owning WM x WN as (WM/16) x (WN/16) MFMA tiles of 16 x 16.
+template <int PAIR, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
+  constexpr int kWavesN = BN / WN;
+  constexpr int kWaves = (BM / WM) * kWavesN;
+  constexpr int TI = WM / 16, TJ = WN / 16;
+  constexpr int kTileA = BM * kBK, kTileB = BN * kBK, kStage = kTileA + kTileB;
+  constexpr bool kBlockScaled = PAIR == kPairBlock || PAIR == kPairBlockK;
+  // per-step scale vectors of the blockwise pairs, staged like the tiles:
+  // A row scales (BM floats) and B scales (the BN/128 weight-block scales,
+  // or BN column scales for 1x128 x 1x128)
+  constexpr int kScaleA = kBlockScaled ? BM * 4 : 0;
+  constexpr int kScaleB = PAIR == kPairBlockK ? BN * 4 : (PAIR == kPairBlock ? 256 : 0);
+  constexpr int kScaleStage = kScaleA + kScaleB;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStage + 2 * kScaleStage + kWaves * 256];
+  uint8_t* const scale_lds = lds + 2 * kStage;
+  uint8_t* const pf_scratch = lds + 2 * kStage + 2 * kScaleStage;
 
   int tm, tn;
-  tile_coords(g.M, g.N, tm, tn);
-  const int64_t m0 = (int64_t)tm * kBM, n0 = (int64_t)tn * kBN;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;  // wave's 64 x 64 sub-tile
+  tile_coords<BM, BN>(g.M, g.N, tm, tn);
+  const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
+  const int lane = threadIdx.x & 63;
+  const int wave = uniform(threadIdx.x >> 6);
+  const int wm = (wave / kWavesN) * WM, wn = (wave % kWavesN) * WN;
   const int KT = (int)(g.K / kBK);
+  const int mw = (int)m0 + wm, nw = (int)n0 + wn;  // wave's first row / column
 
-  v4f acc[4][4];
+  v4f acc[TI][TJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < TJ; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
 
-  // rows of C this lane accumulates: m = m0 + wm + 16 i + lane % 16,
-  // n = n0 + wn + 16 j + 4 (lane / 16) + r
-  int64_t mrow[4];
+  // Scales.  This lane accumulates rows m = mw + 16 i + lane % 16 and
+  // columns n = nw + 16 j + 4 (lane / 16) + r.  Per K block kt the row
+  // scales of A sit at sA[kt * sa_ld + m] (1x128) and the scales of B at
+  // sB[(n / 128) * (K / 128) + kt] (128x128) or sB[kt * sb_ld + n] (1x128).
+  // Reads past the scale arrays return zero through the buffer bounds (they
+  // only feed rows or columns that are never stored).
+  const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.sA, (uint32_t)(g.sa_count * 4));
+  const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.sB, (uint32_t)(g.sb_count * 4));
+  const int kblocks = (int)(g.K / 128);
+  // direct-to-LDS loads of the scale vectors of step kt: instruction q moves
+  // 64 floats; the A vector takes BM / 64 of them, the B vector the rest,
+  // spread round robin over the waves
+  constexpr int kQA = kScaleA / 256, kQB = kScaleB / 256, kQ = kQA + kQB;
+  auto load_scales = [&](int kt, uint8_t* dst) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t m = m0 + wm + i * 16 + (lane & 15);
-    mrow[i] = m < g.M ? m : g.M - 1;
-  }
-  int64_t ncol[4][4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t n = n0 + wn + j * 16 + (lane >> 4) * 4 + r;
-      ncol[j][r] = n < g.N ? n : g.N - 1;
-    }
-
-  // per-K-block scales, fetched one step ahead
-  float sa[4], sb[4][4], sb0 = 0.f;
-  auto fetch_scales = [&](int kt, float (&a)[4], float (&b)[4][4], float& b0) {
-    if (PAIR == kPairBlock || PAIR == kPairBlockK) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = g.sA[(int64_t)kt * g.M + mrow[i]];
-    }
-    if (PAIR == kPairBlock) b0 = g.sB[(n0 / 128) * (g.K / 128) + kt];
-    if (PAIR == kPairBlockK) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) b[j][r] = g.sB[(int64_t)kt * g.N + ncol[j][r]];
+    for (int q = 0; q < kQ; ++q) {
+      if (q % kWaves != wave) continue;
+      if (q < kQA) {
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(dst + q * 256), 4, (q * 64 + lane) * 4,
+                                                 uniform((int)(kt * g.sa_ld + m0) * 4), 0, 0);
+      } else if (PAIR == kPairBlock) {
+        const int blk = (int)(n0 / 128) + lane;  // the tile's BN / 128 weight blocks
+        const int off = lane < BN / 128 ? (blk * kblocks + kt) * 4 : 0x7fffffff;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void*)(dst + kScaleA), 4, off, 0, 0, 0);
+      } else {
+        const int qb = q - kQA;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void*)(dst + kScaleA + qb * 256), 4,
+                                                 (qb * 64 + lane) * 4, uniform((int)(kt * g.sb_ld + n0) * 4),
+                                                 0, 0);
+      }
     }
   };
 
-  fetch_scales(0, sa, sb, sb0);
-  load_tile_lds(g.A, g.lda, m0, g.M, 0, lds);
-  load_tile_lds(g.B, g.ldb, n0, g.N, 0, lds + kTileBytes);
+  const TileLoader<BM, kWaves> ldA(g.A, g.lda, m0, g.M, wave);
+  const TileLoader<BN, kWaves> ldB(g.B, g.ldb, n0, g.N, wave);
+  const LinePrefetcher<BM, BN, kWaves> pf(g.A, g.lda, m0, g.M, g.B, g.ldb, n0, g.N,
+                                          uniform(threadIdx.x >= BM ? 1 : 0) != 0);
+  if (kBlockScaled) load_scales(0, scale_lds);
+  ldA.load(0, lds, wave);
+  ldB.load(0, lds + kTileA, wave);
+  // each step ends its vector-memory issue with one line touch (a dummy one
+  // where no K block is left), so the top-of-step wait can leave it pending
+  pf.touch((KT > 1 ? 1 : 0) * kBK, pf_scratch, wave);
 
+  // a VALU result computed from the last MFMA output of the previous step
+  float done = 0.0f;
   for (int kt = 0; kt < KT; ++kt) {
-    uint8_t* cur = lds + (kt & 1) * kStageBytes;
-    wait_vmem_all();
-    __syncthreads();  // tile kt is in LDS for every wave; stage kt+1 is free
+    uint8_t* cur = lds + (kt & 1) * kStage;
+    uint8_t* cur_scales = scale_lds + (kt & 1) * kScaleStage;
+    wait_vmem_but_one();
+    // Tile kt and its scales are in LDS for every wave (each waited for its
+    // own loads) and stage kt+1 is free (each waited for its LDS reads
+    // before using them).  A bare barrier: __syncthreads() would add a
+    // release fence whose wait also covers the line touch left in flight.
+    asm volatile("s_barrier" ::: "memory");
 
-    float sa_n[4], sb_n[4][4], sb0_n = 0.f;
     if (kt + 1 < KT) {
-      fetch_scales(kt + 1, sa_n, sb_n, sb0_n);
-      uint8_t* nxt = lds + ((kt + 1) & 1) * kStageBytes;
-      load_tile_lds(g.A, g.lda, m0, g.M, (int64_t)(kt + 1) * kBK, nxt);
-      load_tile_lds(g.B, g.ldb, n0, g.N, (int64_t)(kt + 1) * kBK, nxt + kTileBytes);
+      if (kBlockScaled) load_scales(kt + 1, scale_lds + ((kt + 1) & 1) * kScaleStage);
+      uint8_t* nxt = lds + ((kt + 1) & 1) * kStage;
+      ldA.load((kt + 1) * kBK, nxt, wave);
+      ldB.load((kt + 1) * kBK, nxt + kTileA, wave);
+      pf.touch((kt + 2 < KT ? kt + 2 : kt + 1) * kBK, pf_scratch, wave);
     }
 
-    v8i af[4], bf[4];
+    // this step's scales, read from LDS (waited for with the fragments)
+    float sa[TI], sb[TJ][4], sb0 = 0.f;
+    if (kBlockScaled) {
+      const uint32_t a_addr = lds_addr(cur_scales) + (wm + (lane & 15)) * 4;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) af[i] = read_frag(cur, wm + i * 16 + (lane & 15));
+      for (int i = 0; i < TI; ++i) sa[i] = lds_read_f32(a_addr, i * 64);
+    }
+    if (PAIR == kPairBlock) sb0 = lds_read_f32(lds_addr(cur_scales + kScaleA) + (wn / 128) * 4, 0);
+    if (PAIR == kPairBlockK) {
+      const uint32_t b_addr = lds_addr(cur_scales + kScaleA) + (wn + (lane >> 4) * 4) * 4;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bf[j] = read_frag(cur + kTileBytes, wn + j * 16 + (lane & 15));
+      for (int j = 0; j < TJ; ++j) lds_read_f32x4(b_addr + j * 64, sb[j]);
+    }
 
-    if (PAIR == kPairTensor || PAIR == kPairRow) {
+    // Fragment reads: all B fragments of the wave and the A fragments of
+    // the first two row strips, then one wait for all of them.  Every MFMA
+    // of the previous step has completed here: its outputs were consumed by
+    // VALU work (the promotion FMAs, or the `done` product below).
+    const v8i none = {};
+    v8i bf[TJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int j = 0; j < TJ; ++j) bf[j] = read_frag(cur + kTileA, wn + j * 16 + (lane & 15), none, none, done);
+    v8i af = read_frag(cur, wm + (lane & 15), none, none, done);
+    v8i af_next = af;
+    if (TI > 1) af_next = read_frag(cur, wm + 16 + (lane & 15), none, none, done);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = mfma_16x16x128(bf[j], af[i], acc[i][j]);
+    for (int j = 0; j < TJ; ++j) lds_wait<0>(bf[j]);
+    lds_wait<0>(af);
+    lds_wait<0>(af_next);
+    if (kBlockScaled) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i) asm volatile("" : "+v"(sa[i]));
+    }
+    if (PAIR == kPairBlock) asm volatile("" : "+v"(sb0));
+    if (PAIR == kPairBlockK) {
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) asm volatile("" : "+v"(sb[j][r]));
+    }
+
+    if (!kBlockScaled) {
+      // Whole-K accumulation in the MFMA accumulator.  Strip i multiplies
+      // with af; the fragment of strip i+2 is read into registers that are
+      // neither af nor af_next (early clobber against them via `busy`) once
+      // the MFMAs of strip i-1 are done (their output is multiplied into
+      // `done` first), so it never overwrites a source still being read.
+#pragma unroll
+      for (int i = 0; i < TI; ++i) {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
+        v8i af_after = af_next;
+        if (i + 2 < TI) {
+          if (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
+          af_after = read_frag(cur, wm + (i + 2) * 16 + (lane & 15), af, af_next, done);
+          lds_wait<2>(af_next);  // af_next ready; af_after may be in flight
+        } else if (i + 1 < TI) {
+          lds_wait<0>(af_next);  // the last fragment
+        }
+        af = af_next;
+        af_next = af_after;
+      }
+      done = acc[TI - 1][TJ - 1][3] * 0.0f;
     } else {
+      // Row strips of the wave tile, software pipelined: the MFMAs of strip
+      // i+1 (into zeroed partials) are issued before the FMAs that fold the
+      // scaled partials of strip i into the accumulators.  The A fragment of
+      // strip i+2 is read after those FMAs (so the MFMAs of strip i, whose
+      // results they consumed, are done) and away from af_next (still in
+      // use by the MFMAs of strip i+1).  An empty asm makes strip i+1's A
+      // fragment depend on the finished accumulators of strip i-1, so the
+      // compiler cannot hoist later MFMAs: at most two strips of partials
+      // are live, which keeps two waves per SIMD within the register file.
       const v4f zero = {0.f, 0.f, 0.f, 0.f};
+      v4f p[TJ], p_next[TJ];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+      for (int j = 0; j < TJ; ++j) p[j] = mfma_16x16x128(bf[j], af, zero);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const v4f p = mfma_16x16x128(bf[j], af[i], zero);
+      for (int i = 0; i < TI; ++i) {
+        if (i + 1 < TI) {
+          if (i > 0) {
+            order_after(af_next, acc[i - 1]);
+            lds_wait<0>(af_next);  // read during the previous strip
+          }
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) p_next[j] = mfma_16x16x128(bf[j], af_next, zero);
+        }
+        const float si = PAIR == kPairBlock ? sa[i] * sb0 : sa[i];
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            if (PAIR == kPairBlock) {
-              acc[i][j][r] = __builtin_fmaf(p[r], sa[i] * sb0, acc[i][j][r]);
-            } else {
-              acc[i][j][r] = __builtin_fmaf(p[r] * sa[i], sb[j][r], acc[i][j][r]);
-            }
+            if (PAIR == kPairBlock)
+              acc[i][j][r] = __builtin_fmaf(p[j][r], si, acc[i][j][r]);
+            else
+              acc[i][j][r] = __builtin_fmaf(p[j][r] * si, sb[j][r], acc[i][j][r]);
           }
         }
+        if (i + 2 < TI) af_next = read_frag(cur, wm + (i + 2) * 16 + (lane & 15), af_next, af_next, acc[i][TJ - 1][3]);
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) p[j] = p_next[j];
       }
-    }
-
-    if (kt + 1 < KT) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sa[i] = sa_n[i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sb[j][r] = sb_n[j][r];
-      sb0 = sb0_n;
+      done = acc[TI - 1][TJ - 1][3];
     }
   }
 
-  // epilogue: whole-K scales for tensor / row pairs, bf16 RNE, store
+  // Epilogue: whole-K scales for tensor / row pairs, bf16 RNE, then the
+  // tile goes through LDS (the operand stages are free now) so that global
+  // stores are whole 16-byte chunks of contiguous C rows.  LDS row m of the
+  // tile holds BN bf16; its 16-byte chunk c sits at chunk c ^ (m & 15), which
+  // keeps both the 8-byte writes (16 rows, same columns) and the 16-byte
+  // reads (one row) free of bank conflicts.
+  static_assert(BM * BN * 2 <= 2 * kStage, "C tile must fit in the LDS stages");
+  const int voff_m = (lane & 15) * 4, voff_n = (lane >> 4) * 16;
   float st = 1.0f;
-  if (PAIR == kPairTensor) st = g.sA[0] * g.sB[0];
+  if (PAIR == kPairTensor) st = load_f32(rsA, 0, 0) * load_f32(rsB, 0, 0);
+  wait_vmem_all();  // no line touch may still be writing LDS
+  __syncthreads();  // every wave is done with the operand stages
+  constexpr int kRowBytes = BN * 2;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t m = m0 + wm + i * 16 + (lane & 15);
-    if (m >= g.M) continue;
-    const float sm = PAIR == kPairRow ? g.sA[m] : 1.0f;
+  for (int i = 0; i < TI; ++i) {
+    const int mt = wm + i * 16 + (lane & 15);  // row within the tile
+    const float sm = PAIR == kPairRow ? load_f32(rsA, voff_m + i * 64, mw * 4) : 1.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t n = n0 + wn + j * 16 + (lane >> 4) * 4;
+    for (int j = 0; j < TJ; ++j) {
+      const int nt = wn + j * 16 + (lane >> 4) * 4;  // column within the tile
       uint32_t h[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float v = acc[i][j][r];
         if (PAIR == kPairTensor) v = v * st;
-        if (PAIR == kPairRow) v = (v * sm) * g.sB[ncol[j][r]];
+        if (PAIR == kPairRow) v = (v * sm) * load_f32(rsB, voff_n + j * 64 + r * 4, nw * 4);
         h[r] = bf16_rne(v);
       }
-      uint16_t* dst = g.C + m * g.ldc + n;
-      if (n + 3 < g.N) {
-        *reinterpret_cast<uint2*>(dst) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+      const int chunk = (nt * 2) >> 4, half = ((nt * 2) >> 3) & 1;
+      *reinterpret_cast<uint2*>(lds + mt * kRowBytes + ((chunk ^ (mt & 15)) << 4) + half * 8) =
+          make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    }
+  }
+  __syncthreads();
+  constexpr int kChunksPerRow = kRowBytes / 16;
+  constexpr int kThreads = kWaves * 64;
+  constexpr int kRowsPerPass = kThreads / kChunksPerRow;
+  const int c = threadIdx.x % kChunksPerRow;
+  const int64_t n = n0 + c * 8;
+#pragma unroll 4
+  for (int mt = threadIdx.x / kChunksPerRow; mt < BM; mt += kRowsPerPass) {
+    const int64_t m = m0 + mt;
+    if (m >= g.M || n >= g.N) continue;
+    const uint4 v = *reinterpret_cast<const uint4*>(lds + mt * kRowBytes + ((c ^ (mt & 15)) << 4));
+    uint16_t* dst = g.C + m * g.ldc + n;
+    if (n + 8 <= g.N) {
+      if (g.c_aligned16) {
+        *reinterpret_cast<uint4*>(dst) = v;
       } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (n + r < g.N) dst[r] = (uint16_t)h[r];
+        reinterpret_cast<uint2*>(dst)[0] = make_uint2(v.x, v.y);
+        reinterpret_cast<uint2*>(dst)[1] = make_uint2(v.z, v.w);
       }
+    } else {
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+      for (int e = 0; n + e < g.N; ++e) dst[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
     }
   }
 }
 
-}  // namespace
+template <int PAIR, int BM, int BN, int WM, int WN>
+hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
+  constexpr int threads = (BM / WM) * (BN / WN) * 64;
+  gemm_kernel<PAIR, BM, BN, WM, WN><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
+  return hipGetLastError();
+}
+
+// 256 x 256 tiles (8 waves of 128 x 64) when they fill the chip at least
+// twice over; 128 x 128 tiles (4 waves of 64 x 64) otherwise.
+template <int PAIR>
+hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
+  const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  if constexpr (PAIR != kPairBlockK) {
+    if (big_tiles >= 512) return launch_tiles<PAIR, 256, 256, 128, 64>(g, s);
+  }
+  return launch_tiles<PAIR, 128, 128, 64, 64>(g, s);
+}
+
+// The kernels address operands with 32-bit offsets: split the problem into
+// sub-GEMMs whose A and B row ranges each span less than 4 GiB.
+template <int PAIR>
+hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
+  // 32-bit offsets: each sub-problem's A rows and B rows span < 2 GiB, and
+  // row / column indices stay below 2^31 / 4
+  const int64_t lim = (int64_t)1 << 31;
+  int64_t mstep = g.M, nstep = g.N;
+  if (g.M * g.lda >= lim) mstep = ((lim - 1) / g.lda) / 256 * 256;
+  if (g.N * g.ldb >= lim) nstep = ((lim - 1) / g.ldb) / 256 * 256;
+  if (mstep > ((int64_t)1 << 28)) mstep = (int64_t)1 << 28;
+  if (nstep > ((int64_t)1 << 28)) nstep = (int64_t)1 << 28;
+  if (mstep <= 0 || nstep <= 0) return hipErrorInvalidValue;
+  for (int64_t m = 0; m < g.M; m += mstep) {
+    for (int64_t n = 0; n < g.N; n += nstep) {
+      GemmArgs sub = g;
+      sub.M = (g.M - m) < mstep ? (g.M - m) : mstep;
+      sub.N = (g.N - n) < nstep ? (g.N - n) : nstep;
+      sub.A = g.A + m * g.lda;
+      sub.B = g.B + n * g.ldb;
+      sub.C = g.C + m * g.ldc + n;
+      // scale arrays keep the full problem's layout (strides sa_ld, sb_ld);
+      // re-base them at the sub-problem's first row / column
+      int64_t da = 0, db = 0;
+      if (PAIR != kPairTensor) da = m;
+      if (PAIR == kPairRow || PAIR == kPairBlockK) db = n;
+      if (PAIR == kPairBlock) db = (n / 128) * (g.K / 128);
+      sub.sA = g.sA + da;
+      sub.sB = g.sB + db;
+      sub.sa_count = g.sa_count - da;
+      sub.sb_count = g.sb_count - db;
+      hipError_t e = launch_pair<PAIR>(sub, s);
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+// Explicit instantiations: the host pass otherwise emits launch stubs only
+// for the first instantiated pair.
+#define FP8Q_GEMM_KERNEL(PAIR, BM, BN, WM, WN) \
+  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN>(GemmArgs);
+FP8Q_GEMM_KERNEL(kPairTensor, 256, 256, 128, 64)
+FP8Q_GEMM_KERNEL(kPairTensor, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL(kPairRow, 256, 256, 128, 64)
+FP8Q_GEMM_KERNEL(kPairRow, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL(kPairBlock, 256, 256, 128, 64)
+FP8Q_GEMM_KERNEL(kPairBlock, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL(kPairBlockK, 128, 128, 64, 64)
+#undef FP8Q_GEMM_KERNEL
+
+}  // namespace gemm_detail
+
+using namespace gemm_detail;
 
 hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s) {
-  const int64_t tiles = ((g.M + kBM - 1) / kBM) * ((g.N + kBN - 1) / kBN);
-  if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)tiles);
   switch (pair) {
-    case kPairTensor: gemm_kernel<kPairTensor><<<grid, kThreads, 0, s>>>(g); break;
-    case kPairRow: gemm_kernel<kPairRow><<<grid, kThreads, 0, s>>>(g); break;
-    case kPairBlock: gemm_kernel<kPairBlock><<<grid, kThreads, 0, s>>>(g); break;
-    case kPairBlockK: gemm_kernel<kPairBlockK><<<grid, kThreads, 0, s>>>(g); break;
+    case kPairTensor: return launch_split<kPairTensor>(g, s);
+    case kPairRow: return launch_split<kPairRow>(g, s);
+    case kPairBlock: return launch_split<kPairBlock>(g, s);
+    case kPairBlockK: return launch_split<kPairBlockK>(g, s);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace fp8q

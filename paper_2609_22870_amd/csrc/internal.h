@@ -26,6 +26,13 @@ struct GemmArgs {
   const float* sB;
   uint16_t* C;       // bf16 [M][ldc]
   int64_t M, N, K, lda, ldb, ldc;
+  // 1x128 scale layouts [K/128][rows]: distance between K blocks (the row
+  // count of the whole operand, which a sub-problem may not span)
+  int64_t sa_ld, sb_ld;
+  // entries of sA / sB from their base pointers (reads past them are zero)
+  int64_t sa_count, sb_count;
+  // C and ldc allow 16-byte stores (else 8-byte)
+  int c_aligned16;
 };
 
 enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3 };

@@ -17,7 +17,7 @@
 
 namespace fp8q {
 
-namespace {
+namespace quant_detail {
 
 constexpr int kTile = 128;
 constexpr int kThreads = 256;
@@ -288,7 +288,9 @@ hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipS
   return hipGetLastError();
 }
 
-}  // namespace
+}  // namespace quant_detail
+
+using namespace quant_detail;
 
 hipError_t launch_quantize(const QuantArgs& a, int granularity, bool trans, int64_t nscales, hipStream_t s) {
   switch (granularity) {
