@@ -14,6 +14,8 @@
 // The MFMA "A" operand is the B tile (rows n) and the MFMA "B" operand the A
 // tile (rows m): each lane then ends with four consecutive n of one m, which
 // the epilogue stores as one 8-byte bf16x4.
+#include <type_traits>
+
 #include "device_common.h"
 #include "internal.h"
 
@@ -142,18 +144,29 @@ __device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
 // takes those registers), and the
 // address depends on `after`, a VALU result computed from the output of the
 // last MFMA whose source registers may be reused (so that MFMA is done).
-__device__ __forceinline__ v8i read_frag(const uint8_t* lds_tile, int row, const v8i& busy, const v8i& busy2,
-                                         float after) {
-  const int g = (threadIdx.x & 63) >> 4;
-  const int sw = (row >> 1) & 7;
-  uint32_t base = lds_addr(lds_tile) + row * 128;
-  asm volatile("" : "+v"(base) : "v"(after));
-  const uint32_t a_lo = base + (((2 * g) ^ sw) << 4);
-  const uint32_t a_hi = base + (((2 * g + 1) ^ sw) << 4);
+//
+// Fragment rows come in strips of 16 (row = strip base + lane % 16), so the
+// swizzle term (row >> 1) & 7 depends on the lane only: the two chunk
+// addresses are a per-lane constant `lane_off` (low, high) plus the strip's
+// byte offset `imm` (a multiple of 2 KB), which goes into the instruction.
+struct FragAddr {
+  uint32_t lo, hi;  // LDS byte addresses of this lane's two chunks in strip 0
+};
+
+__device__ __forceinline__ FragAddr frag_addr(const uint8_t* lds_tile_strip0) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, r = lane & 15, sw = (r >> 1) & 7;
+  const uint32_t base = lds_addr(lds_tile_strip0) + r * 128;
+  return FragAddr{base + (((2 * g) ^ sw) << 4), base + (((2 * g + 1) ^ sw) << 4)};
+}
+
+template <int IMM>
+__device__ __forceinline__ v8i read_frag(FragAddr a, const v8i& busy, const v8i& busy2, float after) {
+  asm volatile("" : "+v"(a.lo), "+v"(a.hi) : "v"(after));
   uint4 lo, hi;
-  asm volatile("ds_read_b128 %0, %2\n\tds_read_b128 %1, %3"
+  asm volatile("ds_read_b128 %0, %2 offset:%4\n\tds_read_b128 %1, %3 offset:%4"
                : "=&v"(lo), "=&v"(hi)
-               : "v"(a_lo), "v"(a_hi), "v"(busy), "v"(busy2));
+               : "v"(a.lo), "v"(a.hi), "i"(IMM), "v"(busy), "v"(busy2));
   v8i f;
   f[0] = (int)lo.x; f[1] = (int)lo.y; f[2] = (int)lo.z; f[3] = (int)lo.w;
   f[4] = (int)hi.x; f[5] = (int)hi.y; f[6] = (int)hi.z; f[7] = (int)hi.w;
@@ -186,6 +199,14 @@ __device__ __forceinline__ void wait_vmem_all() { asm volatile("s_waitcnt vmcnt(
 __device__ __forceinline__ void wait_vmem_but_one() { asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); }
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+template <int N, typename F, int I = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, F, I + 1>(static_cast<F&&>(f));
+  }
+}
 
 // Empty asm that claims to read `done` and rewrite `next`: whatever consumes
 // `next` afterwards is ordered after everything that produced `done`.
@@ -332,12 +353,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     // of the previous step has completed here: its outputs were consumed by
     // VALU work (the promotion FMAs, or the `done` product below).
     const v8i none = {};
+    const FragAddr fa = frag_addr(cur + wm * 128), fb = frag_addr(cur + kTileA + wn * 128);
     v8i bf[TJ];
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) bf[j] = read_frag(cur + kTileA, wn + j * 16 + (lane & 15), none, none, done);
-    v8i af = read_frag(cur, wm + (lane & 15), none, none, done);
+    static_for<TJ>([&](auto j) { bf[j] = read_frag<j * 2048>(fb, none, none, done); });
+    v8i af = read_frag<0>(fa, none, none, done);
     v8i af_next = af;
-    if (TI > 1) af_next = read_frag(cur, wm + 16 + (lane & 15), none, none, done);
+    if (TI > 1) af_next = read_frag<2048>(fa, none, none, done);
 #pragma unroll
     for (int j = 0; j < TJ; ++j) lds_wait<0>(bf[j]);
     lds_wait<0>(af);
@@ -360,43 +381,49 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       // neither af nor af_next (early clobber against them via `busy`) once
       // the MFMAs of strip i-1 are done (their output is multiplied into
       // `done` first), so it never overwrites a source still being read.
-#pragma unroll
-      for (int i = 0; i < TI; ++i) {
+      static_for<TI>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
 #pragma unroll
         for (int j = 0; j < TJ; ++j) acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
         v8i af_after = af_next;
-        if (i + 2 < TI) {
-          if (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
-          af_after = read_frag(cur, wm + (i + 2) * 16 + (lane & 15), af, af_next, done);
+        if constexpr (i + 2 < TI) {
+          if constexpr (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
+          af_after = read_frag<(i + 2) * 2048>(fa, af, af_next, done);
           lds_wait<2>(af_next);  // af_next ready; af_after may be in flight
-        } else if (i + 1 < TI) {
+        } else if constexpr (i + 1 < TI) {
           lds_wait<0>(af_next);  // the last fragment
         }
         af = af_next;
         af_next = af_after;
-      }
+      });
       done = acc[TI - 1][TJ - 1][3] * 0.0f;
     } else {
       // Row strips of the wave tile, software pipelined: the MFMAs of strip
       // i+1 (into zeroed partials) are issued before the FMAs that fold the
-      // scaled partials of strip i into the accumulators.  The A fragment of
-      // strip i+2 is read after those FMAs (so the MFMAs of strip i, whose
-      // results they consumed, are done) and away from af_next (still in
-      // use by the MFMAs of strip i+1).  An empty asm makes strip i+1's A
-      // fragment depend on the finished accumulators of strip i-1, so the
-      // compiler cannot hoist later MFMAs: at most two strips of partials
-      // are live, which keeps two waves per SIMD within the register file.
+      // scaled partials of strip i into the accumulators.  Three A fragments
+      // rotate: af (strip i, its MFMAs possibly still in flight), af_next
+      // (strip i+1), and the one read at the top of strip i for strip i+2,
+      // into registers away from both and only after the FMAs of strip i-1
+      // consumed the results of its MFMAs (so those are done).  An empty asm
+      // makes strip i+1's A fragment depend on the finished accumulators of
+      // strip i-1, so the compiler cannot hoist later MFMAs: at most two
+      // strips of partials are live, which keeps two waves per SIMD within
+      // the register file.
       const v4f zero = {0.f, 0.f, 0.f, 0.f};
       v4f p[TJ], p_next[TJ];
 #pragma unroll
       for (int j = 0; j < TJ; ++j) p[j] = mfma_16x16x128(bf[j], af, zero);
-#pragma unroll
-      for (int i = 0; i < TI; ++i) {
-        if (i + 1 < TI) {
-          if (i > 0) {
-            order_after(af_next, acc[i - 1]);
-            lds_wait<0>(af_next);  // read during the previous strip
-          }
+      static_for<TI>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        v8i af_after = af_next;
+        if constexpr (i + 2 < TI)
+          af_after = read_frag<(i + 2) * 2048>(fa, af, af_next, i > 0 ? acc[i > 0 ? i - 1 : 0][TJ - 1][3] : done);
+        if constexpr (i + 1 < TI) {
+          if constexpr (i > 0) order_after(af_next, acc[i - 1]);
+          if constexpr (i + 2 < TI)
+            lds_wait<2>(af_next);  // read a strip ago; af_after may be in flight
+          else
+            lds_wait<0>(af_next);
 #pragma unroll
           for (int j = 0; j < TJ; ++j) p_next[j] = mfma_16x16x128(bf[j], af_next, zero);
         }
@@ -411,10 +438,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
               acc[i][j][r] = __builtin_fmaf(p[j][r] * si, sb[j][r], acc[i][j][r]);
           }
         }
-        if (i + 2 < TI) af_next = read_frag(cur, wm + (i + 2) * 16 + (lane & 15), af_next, af_next, acc[i][TJ - 1][3]);
 #pragma unroll
         for (int j = 0; j < TJ; ++j) p[j] = p_next[j];
-      }
+        af = af_next;
+        af_next = af_after;
+      });
       done = acc[TI - 1][TJ - 1][3];
     }
   }
