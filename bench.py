@@ -36,7 +36,47 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=256,
                    help="rows of X the oracle processes for the CPU baseline")
+    p.add_argument("--calibrate-copy-mib", type=int, default=0,
+                   help="after timing, run one plain device-to-device copy of this many "
+                        "MiB: a kernel of known traffic to scale HBM byte counters by")
     return p.parse_args()
+
+
+# Kernel sources whose change invalidates recorded HBM counters.
+GEMM_SOURCES = ["paper_2609_22870_amd/csrc/gemm.hip", "paper_2609_22870_amd/csrc/device_common.h",
+                "paper_2609_22870_amd/csrc/internal.h"]
+
+
+def sources_digest(paths):
+    import hashlib
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload):
+    """HBM bytes per GEMM launch from the committed rocprofv3 counter summary
+    of this workload: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+    multiplied by its copy-kernel calibration factor.  None when there is no
+    summary or the GEMM sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "gemm_%s_counters.md" % workload)
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("    ") and ": " in line:
+                k, v = line.strip().split(": ", 1)
+                rec[k] = v
+    try:
+        if rec["gemm_sources_sha256"] != sources_digest(GEMM_SOURCES):
+            return None
+        return (float(rec["gemm_fetch_kib"]) * float(rec["fetch_factor"]) +
+                float(rec["gemm_write_kib"]) * float(rec["write_factor"])) * 1024.0
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(x, w, M, K, N, rows):
@@ -153,6 +193,8 @@ def main():
     flops = 2.0 * M * N * K
     value = flops / (ms_step * 1e-3) / 1e12
     gemm_tflops = flops / (gemm_ms * 1e-3) / 1e12
+    gemm_bytes = 1.0 * M * K + 1.0 * N * K + 2.0 * M * N + 4.0 * (M * (K // 128) + (N // 128) * (K // 128))
+    traffic = recorded_traffic(args.workload)
     qx_bytes = 3.0 * M * K + 4.0 * M * (K // 128)
     qw_bytes = 3.0 * N * K + 4.0 * (N // 128) * (K // 128)
     out = {
@@ -174,7 +216,8 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(gemm_tflops, 2),
                      "peak": PEAK_FP8_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(gemm_tflops / PEAK_FP8_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": None if traffic is None else round(traffic),
+                     "algorithmic_bytes": round(gemm_bytes)},
         "pct_of_fp8_peak_step": round(100 * value / PEAK_FP8_TFLOPS, 2),
         "kernels_ms": {"quantize_x_1x128": round(qx_ms, 4), "quantize_w_128x128": round(qw_ms, 4),
                        "gemm_blockwise": round(gemm_ms, 4)},
@@ -183,6 +226,13 @@ def main():
                          "hbm_peak": PEAK_HBM_GBS},
         "timed_wall_s": round(wall, 3),
     }
+    if args.calibrate_copy_mib > 0:
+        n = args.calibrate_copy_mib << 20
+        src = torch.zeros(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x.cpu(), w.cpu(), M, K, N, args.cpu_rows)
     print(json.dumps(out), flush=True)

@@ -2,18 +2,24 @@
 //   C[m][n] = sum_k (S_A(m,k) A[m][k]) (S_B(n,k) B[n][k]),  A, B OCP E4M3,
 // fp32 accumulation on the matrix cores, bf16 output.
 //
-// Tiling: a 256-thread workgroup owns a 128 x 128 tile of C; its four waves
-// each own 64 x 64 as 4 x 4 MFMA tiles of 16 x 16.  The K loop steps by 128,
-// which is both the depth of one v_mfma_f32_16x16x128_f8f6f4 and the length
-// of one scale block, so a blockwise step is one MFMA per 16 x 16 tile into
-// a zeroed partial, then one FMA per accumulator that adds S_A * S_B * P.
+// Tiling: a workgroup owns a BM x BN tile of C and steps K by 128, which is
+// both the depth of one v_mfma_f32_16x16x128_f8f6f4 and the length of one
+// scale block, so a blockwise step is one MFMA per 16 x 16 tile into a
+// zeroed partial, then one FMA per accumulator that adds S_A * S_B * P.
+// Two shapes are built: 256 x 256 tiles with eight waves of 128 x 64 (the
+// large-problem kernel: 64 FP8 bytes of LDS traffic per MFMA instead of 128)
+// and 128 x 128 tiles with four waves of 64 x 64 (small grids, and the
+// (1x128, 1x128) pair whose per-column B scales need more registers).
 //
 // Operand tiles (rows x 128 bytes of K) go global -> LDS with the
 // direct-to-LDS 16-byte buffer loads of gfx950 (no VGPR staging), double
-// buffered, XOR-swizzled against LDS bank conflicts.
+// buffered, XOR-swizzled against LDS bank conflicts; the scale vectors of a
+// step travel the same way.  Workgroups are rastered so that the tiles
+// running together on one XCD (which has its own L2) share operand rows.
 // The MFMA "A" operand is the B tile (rows n) and the MFMA "B" operand the A
-// tile (rows m): each lane then ends with four consecutive n of one m, which
-// the epilogue stores as one 8-byte bf16x4.
+// tile (rows m): each lane then ends with four consecutive n of one m.  The
+// epilogue rounds to bf16 and stages the C tile through LDS so that it
+// leaves in 16-byte row segments.
 #include <type_traits>
 
 #include "device_common.h"
@@ -52,11 +58,23 @@ __device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t r, int voff, in
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
 
+// LDS placement of the operand tiles.  Tile row r (128 bytes of K) sits at
+// byte 128 r; its logical 16-byte chunk c sits at physical chunk
+// c ^ chunk_swizzle(r).  The MFMA fragment reads (ds_read_b128) have lane l
+// read row l % 16 of a strip at logical chunk 2 (l / 16) + h.  Measured on
+// gfx950 (64 banks of 4 bytes): a ds_read_b128 goes out in four passes of
+// 16 lanes, a pass being the lanes that agree in lane bit 5 and in the
+// parity of lane bits 2..4, and a pass takes one cycle when its 16 lanes hit
+// 16 different 16-byte bank groups (address bits 4..7), two when two lanes
+// share one, and so on.  The bank group of a fragment read is
+// (row bit 0, c ^ chunk_swizzle(row)); with chunk_swizzle(r) = r1 + 6 r2
+// (bits 1 and 2 of r) the 16 lanes of every pass land on 16 different
+// groups, for both halves h.  (c ^ ((r >> 1) & 7), the swizzle that suits
+// sixteen consecutive lanes, measured two-way conflicted.)
+__device__ __forceinline__ int chunk_swizzle(int r) { return ((r >> 1) & 1) | (((r >> 2) & 1) * 6); }
+
 // Copies of ROWS x 128-byte operand tiles (K bytes k0 .. k0+127) into LDS
-// with direct buffer-to-LDS loads.  In LDS the 16-byte chunk c of tile row r
-// sits at chunk c ^ ((r >> 1) & 7): the LDS has 64 banks (256 bytes), a
-// ds_read_b128 serves 16 lanes at a time, and the 16 rows read together
-// (two per 256 bytes) then hit 16 different 16-byte slots.  A wave
+// with direct buffer-to-LDS loads, in the placement above.  A wave
 // instruction moves a group of eight rows: lane l lands at byte 16 l of the
 // group's 1 KB, i.e. row l / 8, physical chunk l % 8, so it fetches the
 // logical chunk that maps there.  Each
@@ -76,10 +94,10 @@ struct TileLoader {
     rsrc = make_rsrc(base, (uint32_t)(rows * ld));
     const int lane = threadIdx.x & 63;
     const int trow = wave * kPerWave * 8 + (lane >> 3);  // tile row of group 0 (kPerWave even)
-    // the chunk swizzle depends on (trow >> 1) & 7, which differs between
-    // even and odd groups only
-    const int chunk_even = (lane & 7) ^ ((trow >> 1) & 7);
-    const int chunk_odd = (lane & 7) ^ (((trow + 8) >> 1) & 7);
+    // the chunk swizzle repeats every 16 rows: even groups share one value,
+    // odd groups another
+    const int chunk_even = (lane & 7) ^ chunk_swizzle(trow);
+    const int chunk_odd = (lane & 7) ^ chunk_swizzle(trow + 8);
     const int64_t r = row0 + trow;
     // rows past the operand give offsets past the buffer: they read zero
     off_even = (int)(r * ld) + chunk_even * 16;
@@ -146,7 +164,7 @@ __device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
 // last MFMA whose source registers may be reused (so that MFMA is done).
 //
 // Fragment rows come in strips of 16 (row = strip base + lane % 16), so the
-// swizzle term (row >> 1) & 7 depends on the lane only: the two chunk
+// swizzle term chunk_swizzle(row) depends on the lane only: the two chunk
 // addresses are a per-lane constant `lane_off` (low, high) plus the strip's
 // byte offset `imm` (a multiple of 2 KB), which goes into the instruction.
 struct FragAddr {
@@ -155,7 +173,7 @@ struct FragAddr {
 
 __device__ __forceinline__ FragAddr frag_addr(const uint8_t* lds_tile_strip0) {
   const int lane = threadIdx.x & 63;
-  const int g = lane >> 4, r = lane & 15, sw = (r >> 1) & 7;
+  const int g = lane >> 4, r = lane & 15, sw = chunk_swizzle(r);
   const uint32_t base = lds_addr(lds_tile_strip0) + r * 128;
   return FragAddr{base + (((2 * g) ^ sw) << 4), base + (((2 * g + 1) ^ sw) << 4)};
 }
