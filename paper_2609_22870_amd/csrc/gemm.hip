@@ -71,6 +71,15 @@ __device__ __forceinline__ float load_f32(__amdgpu_buffer_rsrc_t r, int voff, in
 // (bits 1 and 2 of r) the 16 lanes of every pass land on 16 different
 // groups, for both halves h.  (c ^ ((r >> 1) & 7), the swizzle that suits
 // sixteen consecutive lanes, measured two-way conflicted.)
+// Calls f(integral_constant<int, I>) for I = 0 .. N-1, unrolled.
+template <int N, typename F, int I = 0>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, F, I + 1>(static_cast<F&&>(f));
+  }
+}
+
 __device__ __forceinline__ int chunk_swizzle(int r) { return ((r >> 1) & 1) | (((r >> 2) & 1) * 6); }
 
 // Copies of ROWS x 128-byte operand tiles (K bytes k0 .. k0+127) into LDS
@@ -105,40 +114,15 @@ struct TileLoader {
     step = (int)(16 * ld);
   }
 
+  // the wave's row group G (of kPerWave)
+  template <int G>
+  __device__ __forceinline__ void load_group(int k0, uint8_t* lds_tile, int wave) const {
+    const int off = (G & 1 ? off_odd : off_even) + (G >> 1) * step;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_tile + (wave * kPerWave + G) * 1024), 16, off,
+                                             k0, 0, 0);
+  }
   __device__ __forceinline__ void load(int k0, uint8_t* lds_tile, int wave) const {
-#pragma unroll
-    for (int g = 0; g < kPerWave; ++g) {
-      const int off = (g & 1 ? off_odd : off_even) + (g >> 1) * step;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds_tile + (wave * kPerWave + g) * 1024), 16,
-                                               off, k0, 0, 0);
-    }
-  }
-};
-
-// Touches every 128-byte line of one K block of the A and B tiles with a
-// 4-byte direct-to-LDS load into a scratch corner of LDS: the lines are
-// pulled into L2 one K step before the tile loads fetch them, which then hit
-// L2 instead of waiting on memory.  No VGPR is involved, so the loads can
-// stay outstanding across a step.
-template <int BM, int BN, int NWAVES>
-struct LinePrefetcher {
-  static constexpr int kLines = BM + BN;
-  static_assert(kLines == NWAVES * 64, "one line per lane");
-  __amdgpu_buffer_rsrc_t rsrc;
-  int off;
-
-  __device__ __forceinline__ LinePrefetcher(const uint8_t* A, int64_t lda, int64_t m0, int64_t M,
-                                            const uint8_t* B, int64_t ldb, int64_t n0, int64_t N,
-                                            bool is_b) {
-    const int t = threadIdx.x;
-    const int64_t r = is_b ? n0 + (t - BM) : m0 + t;
-    const int64_t rows = is_b ? N : M, ld = is_b ? ldb : lda;
-    rsrc = make_rsrc(is_b ? B : A, (uint32_t)(rows * ld));
-    off = r < rows ? (int)(r * ld) : (int)0x7fffffff;
-  }
-
-  __device__ __forceinline__ void touch(int k0, uint8_t* scratch, int wave) const {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(scratch + wave * 256), 4, off, k0, 0, 0);
+    static_for<kPerWave>([&](auto g) { load_group<decltype(g)::value>(k0, lds_tile, wave); });
   }
 };
 
@@ -212,19 +196,19 @@ __device__ __forceinline__ void lds_wait(v8i& f) {
   asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(f) : "n"(N));
 }
 
+// No instruction may be scheduled across this point: it pins the matrix
+// instructions next to the (inline asm) LDS waits they depend on.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+template <int N>
+__device__ __forceinline__ void lds_wait2(v8i& f, v8i& h) {
+  asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(f), "+v"(h) : "n"(N));
+}
+
 __device__ __forceinline__ void wait_vmem_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-// all but the last vector-memory instruction of this wave have completed
-__device__ __forceinline__ void wait_vmem_but_one() { asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); }
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
-template <int N, typename F, int I = 0>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    static_for<N, F, I + 1>(static_cast<F&&>(f));
-  }
-}
 
 // Empty asm that claims to read `done` and rewrite `next`: whatever consumes
 // `next` afterwards is ordered after everything that produced `done`.
@@ -271,7 +255,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   constexpr int kScaleStage = kScaleA + kScaleB;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStage + 2 * kScaleStage + kWaves * 256];
   uint8_t* const scale_lds = lds + 2 * kStage;
-  uint8_t* const pf_scratch = lds + 2 * kStage + 2 * kScaleStage;
+  uint8_t* const dummy_lds = lds + 2 * kStage + 2 * kScaleStage;  // 256 bytes per wave
 
   int tm, tn;
   tile_coords<BM, BN>(g.M, g.N, tm, tn);
@@ -298,102 +282,145 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.sB, (uint32_t)(g.sb_count * 4));
   const int kblocks = (int)(g.K / 128);
   // direct-to-LDS loads of the scale vectors of step kt: instruction q moves
-  // 64 floats; the A vector takes BM / 64 of them, the B vector the rest,
-  // spread round robin over the waves
+  // 64 floats; the A vector takes BM / 64 of them, the B vector the rest.
+  // Wave q issues instruction q, without branching: the waves past kQ issue
+  // a load whose offset is past the buffer (it reads zeros) into their own
+  // 256-byte dummy corner of LDS.
   constexpr int kQA = kScaleA / 256, kQB = kScaleB / 256, kQ = kQA + kQB;
-  auto load_scales = [&](int kt, uint8_t* dst) {
-#pragma unroll
-    for (int q = 0; q < kQ; ++q) {
-      if (q % kWaves != wave) continue;
-      if (q < kQA) {
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsA, (lds_void*)(dst + q * 256), 4, (q * 64 + lane) * 4,
-                                                 uniform((int)(kt * g.sa_ld + m0) * 4), 0, 0);
-      } else if (PAIR == kPairBlock) {
-        const int blk = (int)(n0 / 128) + lane;  // the tile's BN / 128 weight blocks
-        const int off = lane < BN / 128 ? (blk * kblocks + kt) * 4 : 0x7fffffff;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void*)(dst + kScaleA), 4, off, 0, 0, 0);
-      } else {
-        const int qb = q - kQA;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsB, (lds_void*)(dst + kScaleA + qb * 256), 4,
-                                                 (qb * 64 + lane) * 4, uniform((int)(kt * g.sb_ld + n0) * 4),
-                                                 0, 0);
-      }
+  const bool q_is_a = wave < kQA;
+  const __amdgpu_buffer_rsrc_t rs_q = q_is_a ? rsA : rsB;
+  int q_dst = 0, q_voff = 0x7fffffff, q_ld = 0, q_base = 0;
+  if (wave < kQA) {
+    q_dst = wave * 256;
+    q_voff = (wave * 64 + lane) * 4;
+    q_ld = (int)g.sa_ld * 4;
+    q_base = (int)m0 * 4;
+  } else if (wave < kQ) {
+    q_dst = kScaleA + (wave - kQA) * 256;
+    if (PAIR == kPairBlock) {
+      // the tile's BN / 128 weight blocks, each with K / 128 scales
+      q_voff = lane < BN / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
+      q_ld = 4;
+    } else {
+      q_voff = ((wave - kQA) * 64 + lane) * 4;
+      q_ld = (int)g.sb_ld * 4;
+      q_base = (int)n0 * 4;
     }
+  }
+  q_dst = uniform(q_dst);
+  q_ld = uniform(q_ld);
+  q_base = uniform(q_base);
+  // LDS destination per stage (0, 1) of this wave's instruction
+  uint8_t* const q_to0 = wave < kQ ? scale_lds + q_dst : dummy_lds + wave * 256;
+  uint8_t* const q_to1 = wave < kQ ? scale_lds + kScaleStage + q_dst : dummy_lds + wave * 256;
+  auto load_scales = [&](int kt) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_void*)(kt & 1 ? q_to1 : q_to0), 4, q_voff,
+                                             q_base + kt * q_ld, 0, 0);
   };
 
   const TileLoader<BM, kWaves> ldA(g.A, g.lda, m0, g.M, wave);
   const TileLoader<BN, kWaves> ldB(g.B, g.ldb, n0, g.N, wave);
-  const LinePrefetcher<BM, BN, kWaves> pf(g.A, g.lda, m0, g.M, g.B, g.ldb, n0, g.N,
-                                          uniform(threadIdx.x >= BM ? 1 : 0) != 0);
-  if (kBlockScaled) load_scales(0, scale_lds);
+  if constexpr (kBlockScaled) load_scales(0);
   ldA.load(0, lds, wave);
   ldB.load(0, lds + kTileA, wave);
-  // each step ends its vector-memory issue with one line touch (a dummy one
-  // where no K block is left), so the top-of-step wait can leave it pending
-  pf.touch((KT > 1 ? 1 : 0) * kBK, pf_scratch, wave);
 
   // a VALU result computed from the last MFMA output of the previous step
   float done = 0.0f;
-  for (int kt = 0; kt < KT; ++kt) {
+  // The vector-memory work of a step (the loads of stage kt+1) is a list of
+  // kSlots direct-to-LDS instructions per wave: its scale-vector load (for
+  // the blockwise pairs; waves past kQ have none), its A row groups, its B
+  // row groups.  They go out two or three per row strip,
+  // between the matrix instructions: issued all at once they would stall the
+  // wave on the vector-memory queue, which drains at about 64 bytes per clock
+  // per CU.
+  constexpr int kPerA = TileLoader<BM, kWaves>::kPerWave, kPerB = TileLoader<BN, kWaves>::kPerWave;
+  constexpr int kS0 = kBlockScaled ? 1 : 0;
+  constexpr int kSlots = kS0 + kPerA + kPerB;
+  constexpr int kPerStrip = (kSlots + TI - 1) / TI > 2 ? (kSlots + TI - 1) / TI : 2;
+  static_assert(kQ <= kWaves, "at most one scale-vector load per wave and step");
+  // LDS reads of the step's scales, issued after the first strip's MFMAs
+  constexpr int kScaleReads = PAIR == kPairBlock ? TI + 1 : (PAIR == kPairBlockK ? TI + TJ : 0);
+  static_assert(kScaleReads + 2 <= 15, "outstanding LDS reads must fit the lgkm counter");
+
+  // One K step; kMore: the loads of stage kt+1 go out during it (all but
+  // the last step, which is peeled so that no step carries a branch).
+  auto step = [&](const int kt, auto more_c) __attribute__((always_inline)) {
+    constexpr bool kMore = decltype(more_c)::value;
     uint8_t* cur = lds + (kt & 1) * kStage;
     uint8_t* cur_scales = scale_lds + (kt & 1) * kScaleStage;
-    wait_vmem_but_one();
+    uint8_t* nxt = lds + ((kt + 1) & 1) * kStage;
+    wait_vmem_all();
     // Tile kt and its scales are in LDS for every wave (each waited for its
     // own loads) and stage kt+1 is free (each waited for its LDS reads
     // before using them).  A bare barrier: __syncthreads() would add a
-    // release fence whose wait also covers the line touch left in flight.
+    // release fence (a wait the loads above already made).
     asm volatile("s_barrier" ::: "memory");
+    // the vector-memory slots of strip I
+    auto issue_strip = [&](auto ic) {
+      constexpr int I = decltype(ic)::value;
+      if constexpr (kMore) static_for<kSlots>([&](auto sc) {
+        constexpr int S = decltype(sc)::value;
+        if constexpr (S >= I * kPerStrip && S < (I + 1) * kPerStrip) {
+          if constexpr (S < kS0)
+            load_scales(kt + 1);
+          else if constexpr (S - kS0 < kPerA)
+            ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>((kt + 1) * kBK, nxt, wave);
+          else
+            ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>((kt + 1) * kBK, nxt + kTileA, wave);
+        }
+      });
+    };
 
-    if (kt + 1 < KT) {
-      if (kBlockScaled) load_scales(kt + 1, scale_lds + ((kt + 1) & 1) * kScaleStage);
-      uint8_t* nxt = lds + ((kt + 1) & 1) * kStage;
-      ldA.load((kt + 1) * kBK, nxt, wave);
-      ldB.load((kt + 1) * kBK, nxt + kTileA, wave);
-      pf.touch((kt + 2 < KT ? kt + 2 : kt + 1) * kBK, pf_scratch, wave);
-    }
-
-    // this step's scales, read from LDS (waited for with the fragments)
-    float sa[TI], sb[TJ][4], sb0 = 0.f;
-    if (kBlockScaled) {
-      const uint32_t a_addr = lds_addr(cur_scales) + (wm + (lane & 15)) * 4;
-#pragma unroll
-      for (int i = 0; i < TI; ++i) sa[i] = lds_read_f32(a_addr, i * 64);
-    }
-    if (PAIR == kPairBlock) sb0 = lds_read_f32(lds_addr(cur_scales + kScaleA) + (wn / 128) * 4, 0);
-    if (PAIR == kPairBlockK) {
-      const uint32_t b_addr = lds_addr(cur_scales + kScaleA) + (wn + (lane >> 4) * 4) * 4;
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) lds_read_f32x4(b_addr + j * 64, sb[j]);
-    }
-
-    // Fragment reads: all B fragments of the wave and the A fragments of
-    // the first two row strips, then one wait for all of them.  Every MFMA
-    // of the previous step has completed here: its outputs were consumed by
-    // VALU work (the promotion FMAs, or the `done` product below).
+    // Fragment reads of the first two strips: A strip 0, the B fragments,
+    // A strip 1.  The MFMAs of strip 0 each wait only for their own B
+    // fragment.  Every MFMA of the previous step has completed here: its
+    // outputs were consumed by VALU work (the promotion FMAs, or the `done`
+    // product below), which the reads' addresses depend on.
     const v8i none = {};
     const FragAddr fa = frag_addr(cur + wm * 128), fb = frag_addr(cur + kTileA + wn * 128);
+    v8i af = read_frag<0>(fa, none, none, done);
     v8i bf[TJ];
     static_for<TJ>([&](auto j) { bf[j] = read_frag<j * 2048>(fb, none, none, done); });
-    v8i af = read_frag<0>(fa, none, none, done);
     v8i af_next = af;
-    if (TI > 1) af_next = read_frag<2048>(fa, none, none, done);
-#pragma unroll
-    for (int j = 0; j < TJ; ++j) lds_wait<0>(bf[j]);
-    lds_wait<0>(af);
-    lds_wait<0>(af_next);
-    if (kBlockScaled) {
-#pragma unroll
-      for (int i = 0; i < TI; ++i) asm volatile("" : "+v"(sa[i]));
-    }
-    if (PAIR == kPairBlock) asm volatile("" : "+v"(sb0));
-    if (PAIR == kPairBlockK) {
-#pragma unroll
-      for (int j = 0; j < TJ; ++j)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) asm volatile("" : "+v"(sb[j][r]));
-    }
+    if constexpr (TI > 1) af_next = read_frag<2048>(fa, none, none, done);
+    constexpr int kNextReads = TI > 1 ? 2 : 0;
+    auto wait_b = [&](auto jc) {  // before strip 0's MFMA with B fragment j
+      constexpr int j = decltype(jc)::value;
+      if constexpr (j == 0)
+        lds_wait2<2 * (TJ - 1) + kNextReads>(af, bf[0]);
+      else
+        lds_wait<2 * (TJ - 1 - j) + kNextReads>(bf[j]);
+    };
 
-    if (!kBlockScaled) {
+    float sa[TI], sb[TJ][4], sb0 = 0.f;
+    auto read_scales = [&]() {
+      if (kBlockScaled) {
+        const uint32_t a_addr = lds_addr(cur_scales) + (wm + (lane & 15)) * 4;
+#pragma unroll
+        for (int i = 0; i < TI; ++i) sa[i] = lds_read_f32(a_addr, i * 64);
+      }
+      if (PAIR == kPairBlock) sb0 = lds_read_f32(lds_addr(cur_scales + kScaleA) + (wn / 128) * 4, 0);
+      if (PAIR == kPairBlockK) {
+        const uint32_t b_addr = lds_addr(cur_scales + kScaleA) + (wn + (lane >> 4) * 4) * 4;
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) lds_read_f32x4(b_addr + j * 64, sb[j]);
+      }
+    };
+    auto scales_ready = [&]() {  // after an lgkm wait that covers the scale reads
+      if (kBlockScaled) {
+#pragma unroll
+        for (int i = 0; i < TI; ++i) asm volatile("" : "+v"(sa[i]));
+      }
+      if (PAIR == kPairBlock) asm volatile("" : "+v"(sb0));
+      if (PAIR == kPairBlockK) {
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) asm volatile("" : "+v"(sb[j][r]));
+      }
+    };
+
+    if constexpr (!kBlockScaled) {
       // Whole-K accumulation in the MFMA accumulator.  Strip i multiplies
       // with af; the fragment of strip i+2 is read into registers that are
       // neither af nor af_next (early clobber against them via `busy`) once
@@ -401,8 +428,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       // `done` first), so it never overwrites a source still being read.
       static_for<TI>([&](auto ic) {
         constexpr int i = decltype(ic)::value;
-#pragma unroll
-        for (int j = 0; j < TJ; ++j) acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
+        static_for<TJ>([&](auto jc) {
+          constexpr int j = decltype(jc)::value;
+          if constexpr (i == 0) wait_b(jc);
+          acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
+          if constexpr (i == 0) sched_fence();
+        });
+        issue_strip(ic);
+        sched_fence();
         v8i af_after = af_next;
         if constexpr (i + 2 < TI) {
           if constexpr (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
@@ -429,21 +462,32 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       // the register file.
       const v4f zero = {0.f, 0.f, 0.f, 0.f};
       v4f p[TJ], p_next[TJ];
-#pragma unroll
-      for (int j = 0; j < TJ; ++j) p[j] = mfma_16x16x128(bf[j], af, zero);
+      static_for<TJ>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        wait_b(jc);
+        p[j] = mfma_16x16x128(bf[j], af, zero);
+        sched_fence();
+      });
+      read_scales();
       static_for<TI>([&](auto ic) {
         constexpr int i = decltype(ic)::value;
+        constexpr int kAfter = i + 2 < TI ? 2 : 0;  // reads of af_after
         v8i af_after = af_next;
         if constexpr (i + 2 < TI)
           af_after = read_frag<(i + 2) * 2048>(fa, af, af_next, i > 0 ? acc[i > 0 ? i - 1 : 0][TJ - 1][3] : done);
         if constexpr (i + 1 < TI) {
           if constexpr (i > 0) order_after(af_next, acc[i - 1]);
-          if constexpr (i + 2 < TI)
-            lds_wait<2>(af_next);  // read a strip ago; af_after may be in flight
-          else
-            lds_wait<0>(af_next);
+          // af_next was read before the scales (strip 0) or a strip ago
+          lds_wait<kAfter + (i == 0 ? kScaleReads : 0)>(af_next);
 #pragma unroll
           for (int j = 0; j < TJ; ++j) p_next[j] = mfma_16x16x128(bf[j], af_next, zero);
+        }
+        sched_fence();
+        issue_strip(ic);
+        sched_fence();
+        if constexpr (i == 0) {
+          asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(kAfter));
+          scales_ready();
         }
         const float si = PAIR == kPairBlock ? sa[i] * sb0 : sa[i];
 #pragma unroll
@@ -463,7 +507,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       });
       done = acc[TI - 1][TJ - 1][3];
     }
-  }
+  };
+  for (int kt = 0; kt + 1 < KT; ++kt) step(kt, std::true_type{});
+  step(KT - 1, std::false_type{});
 
   // Epilogue: whole-K scales for tensor / row pairs, bf16 RNE, then the
   // tile goes through LDS (the operand stages are free now) so that global
@@ -475,7 +521,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const int voff_m = (lane & 15) * 4, voff_n = (lane >> 4) * 16;
   float st = 1.0f;
   if (PAIR == kPairTensor) st = load_f32(rsA, 0, 0) * load_f32(rsB, 0, 0);
-  wait_vmem_all();  // no line touch may still be writing LDS
+  wait_vmem_all();  // no load may still be writing LDS
   __syncthreads();  // every wave is done with the operand stages
   constexpr int kRowBytes = BN * 2;
 #pragma unroll
