@@ -329,14 +329,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // The vector-memory work of a step (the loads of stage kt+1) is a list of
   // kSlots direct-to-LDS instructions per wave: its scale-vector load (for
   // the blockwise pairs; waves past kQ have none), its A row groups, its B
-  // row groups.  They go out two or three per row strip,
+  // row groups.  They go out two or three at a time,
   // between the matrix instructions: issued all at once they would stall the
   // wave on the vector-memory queue, which drains at about 64 bytes per clock
   // per CU.
   constexpr int kPerA = TileLoader<BM, kWaves>::kPerWave, kPerB = TileLoader<BN, kWaves>::kPerWave;
   constexpr int kS0 = kBlockScaled ? 1 : 0;
   constexpr int kSlots = kS0 + kPerA + kPerB;
-  constexpr int kPerStrip = (kSlots + TI - 1) / TI > 2 ? (kSlots + TI - 1) / TI : 2;
+  // kPre slots go out right after the barrier, while the wave waits for its
+  // first fragments; the rest kPerStrip per strip
+  constexpr int kPre = TI >= 8 ? 2 : 0;
+  constexpr int kPerStrip = (kSlots - kPre + TI - 1) / TI > 2 ? (kSlots - kPre + TI - 1) / TI : 2;
   static_assert(kQ <= kWaves, "at most one scale-vector load per wave and step");
   // LDS reads of the step's scales, issued after the first strip's MFMAs
   constexpr int kScaleReads = PAIR == kPairBlock ? TI + 1 : (PAIR == kPairBlockK ? TI + TJ : 0);
@@ -360,7 +363,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       constexpr int I = decltype(ic)::value;
       if constexpr (kMore) static_for<kSlots>([&](auto sc) {
         constexpr int S = decltype(sc)::value;
-        if constexpr (S >= I * kPerStrip && S < (I + 1) * kPerStrip) {
+        if constexpr (I < 0 ? S < kPre : (S >= kPre + I * kPerStrip && S < kPre + (I + 1) * kPerStrip)) {
           if constexpr (S < kS0)
             load_scales(kt + 1);
           else if constexpr (S - kS0 < kPerA)
@@ -384,6 +387,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     v8i af_next = af;
     if constexpr (TI > 1) af_next = read_frag<2048>(fa, none, none, done);
     constexpr int kNextReads = TI > 1 ? 2 : 0;
+    issue_strip(std::integral_constant<int, -1>{});
     auto wait_b = [&](auto jc) {  // before strip 0's MFMA with B fragment j
       constexpr int j = decltype(jc)::value;
       if constexpr (j == 0)
