@@ -39,12 +39,14 @@ __device__ __forceinline__ UnitScale unit_scale(float amax) {
 // is taken as q0 S - x, not x - q0 S, so that x = -0 keeps its sign: the
 // exact zero residual is +0 and -(+0) r + (-0) = -0.  Smaller S take the
 // IEEE division.
+__device__ __forceinline__ float fast_quotient(float x, float s, float r) {
+  const float q0 = x * r;
+  const float e = __builtin_fmaf(q0, s, -x);
+  return __builtin_fmaf(-e, r, q0);
+}
+
 __device__ __forceinline__ float quotient(float x, const UnitScale& u) {
-  if (u.fast) {
-    float q0 = x * u.r;
-    float e = __builtin_fmaf(q0, u.s, -x);
-    return __builtin_fmaf(-e, u.r, q0);
-  }
+  if (u.fast) return fast_quotient(x, u.s, u.r);
   return x / u.s;
 }
 

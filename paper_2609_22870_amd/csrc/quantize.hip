@@ -20,6 +20,7 @@ namespace fp8q {
 namespace quant_detail {
 
 constexpr int kTile = 128;
+constexpr int kWideRows = 32, kWideCols = 512;
 constexpr int kThreads = 256;
 
 enum Kind { kBlock1x128, kBlock128x1, kBlock128x128, kPreTensor, kPreRow, kPreCol };
@@ -28,14 +29,13 @@ struct Tile {
   float v[8][8];  // [row i][column j] of this thread's 8 x 8 patch
 };
 
-__device__ __forceinline__ void load_tile(const QuantArgs& a, int64_t r0, int64_t c0, Tile& t) {
-  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  const int64_t c = c0 + cc * 8;
+// Rows row0 .. row0+7, columns c .. c+7 of x (zeros outside).
+__device__ __forceinline__ void load_patch(const QuantArgs& a, int64_t row0, int64_t c, Tile& t) {
   const bool col_ok = c < a.cols;
   uint4 w[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const int64_t r = r0 + rg * 8 + i;
+    const int64_t r = row0 + i;
     w[i] = make_uint4(0u, 0u, 0u, 0u);
     if (col_ok && r < a.rows) w[i] = *reinterpret_cast<const uint4*>(a.x + r * a.ldx + c);
   }
@@ -93,71 +93,136 @@ __device__ __forceinline__ float tile_max(const Tile& t, float* lds4) {
   return fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3]));
 }
 
+// The quotient for units of any scale, out of line: only waves holding a
+// unit with S < 2^-90 call it, and keeping its IEEE divisions out of the
+// kernel body keeps the common path's register use low.
+__device__ __noinline__ float slow_quotient(float x, float s, float r) {
+  return quotient(x, UnitScale{s, r, s >= 0x1p-90f});
+}
+
 template <int K, bool TRANS>
 __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   __shared__ float lds_red[4 * kTile];
   __shared__ uint64_t lds_t[TRANS ? kTile * kTile / 8 : 1];
 
+  // Row units without transposition use wide tiles of 32 x 512: wave w
+  // takes rows 8 w .. 8 w + 7 and each load instruction reads one row's
+  // 1 KB (four 128-column blocks, one per 16-lane group).  The others use
+  // 128 x 128 tiles: thread (rg, cc) takes rows 8 rg .. 8 rg + 7.  Either
+  // way a thread holds 8 rows x 8 columns, and the 16 lanes of a DPP row
+  // share the thread's rows and cover 128 consecutive columns.
+  constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow);
   const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  const int64_t r0 = (int64_t)blockIdx.y * kTile;
-  const int64_t c0 = (int64_t)blockIdx.x * kTile;
-  const int64_t c = c0 + cc * 8;
+  const int64_t tr = blockIdx.y, tc = blockIdx.x, tiles_r = gridDim.y, tiles_c = gridDim.x;
+  const int64_t r0 = tr * (kWide ? kWideRows : kTile);
+  const int64_t c0 = tc * (kWide ? kWideCols : kTile);
+  const int64_t row0 = kWide ? r0 + (threadIdx.x >> 6) * 8 : r0 + rg * 8;  // first of the thread's rows
+  const int64_t c = kWide ? c0 + ((threadIdx.x >> 4) & 3) * 128 + cc * 8 : c0 + cc * 8;
 
   Tile t;
-  load_tile(a, r0, c0, t);
+  load_patch(a, row0, c, t);
 
-  // Per-unit scales for this thread's elements: by row (1x128, ROW),
-  // by column (128x1, COL), or one per tile (128x128, TENSOR).
-  UnitScale us[8];
-  if (K == kBlock1x128) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) us[i] = unit_scale(row16_max(row_partial_max(t, i)));
-  } else if (K == kBlock128x1) {
-    float m[8];
-    tile_col_max(t, lds_red, m);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) us[j] = unit_scale(m[j]);
-  } else if (K == kBlock128x128) {
-    us[0] = unit_scale(tile_max(t, lds_red));
-  } else if (K == kPreTensor) {
-    us[0] = unit_scale(a.scales[0]);
-  } else if (K == kPreRow) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int64_t r = r0 + rg * 8 + i;
-      us[i] = unit_scale(r < a.rows ? a.scales[r] : 0.0f);
-    }
-  } else {  // kPreCol
-#pragma unroll
-    for (int j = 0; j < 8; ++j) us[j] = unit_scale(c + j < a.cols ? a.scales[c + j] : 0.0f);
-  }
-
+  // Per-unit scales.  A thread's elements belong to eight units (its rows for
+  // 1x128 and ROW, its columns for 128x1 and COL) or to one (128x128,
+  // TENSOR).  In the eight-unit case each unit's S and 1/S (two IEEE
+  // divisions) are computed once, by one of the threads that share the unit,
+  // and handed to the others: for rows, lane cc of a 16-lane row group
+  // computes row cc % 8 and the group exchanges by lane shuffles; for
+  // columns, thread (rg, cc) with rg < 8 computes column 8 cc + rg and the
+  // block exchanges through LDS.
   constexpr bool by_row = K == kBlock1x128 || K == kPreRow;
   constexpr bool by_col = K == kBlock128x1 || K == kPreCol;
+  const int lane = threadIdx.x & 63;
+  UnitScale mine;  // the unit this thread computes (eight-unit case)
+  float su[8], ru[8];
+  if (by_row) {
+    float amax;
+    if (K == kBlock1x128) {
+      float am[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) am[i] = row16_max(row_partial_max(t, i));
+      amax = am[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) amax = (cc & 7) == i ? am[i] : amax;
+    } else {
+      const int64_t r = row0 + (cc & 7);
+      amax = r < a.rows ? a.scales[r] : 0.0f;
+    }
+    mine = unit_scale(amax);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      su[i] = __shfl(mine.s, (lane & 48) | i, 64);
+      ru[i] = __shfl(mine.r, (lane & 48) | i, 64);
+    }
+  } else if (by_col) {
+    float amax;
+    if (K == kBlock128x1) {
+      float m[8];
+      tile_col_max(t, lds_red, m);
+      amax = m[0];
+#pragma unroll
+      for (int j = 1; j < 8; ++j) amax = (rg & 7) == j ? m[j] : amax;
+    } else {
+      const int64_t cj = c0 + cc * 8 + (rg & 7);
+      amax = cj < a.cols ? a.scales[cj] : 0.0f;
+    }
+    mine = unit_scale(amax);
+    // exchange through LDS (after tile_col_max's reads of lds_red are done)
+    float2* lds_su = reinterpret_cast<float2*>(lds_red + 2 * kTile);
+    __syncthreads();
+    if (rg < 8) lds_su[cc * 8 + rg] = make_float2(mine.s, mine.r);
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float2 v = lds_su[cc * 8 + j];
+      su[j] = v.x;
+      ru[j] = v.y;
+    }
+  } else {
+    mine = unit_scale(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0]);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      su[i] = mine.s;
+      ru[i] = mine.r;
+    }
+  }
+
+  // The reciprocal-based quotient holds for S >= 2^-90 (see quotient());
+  // waves whose units all satisfy it take the branch-free path.
+  bool fast = true;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) fast = fast && su[i] >= 0x1p-90f;
+  const bool wave_fast = __all(fast);
 
   // codes, two E4M3 bytes per conversion; q[i][j] -> byte j of row i
   uint32_t packed[8][2];
+  auto encode_all = [&](auto qf) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < 8; ++i) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      float q[4];
+      for (int h = 0; h < 2; ++h) {
+        float q[4];
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const int j = h * 4 + jj;
-        const UnitScale& u = by_row ? us[i] : (by_col ? us[j] : us[0]);
-        q[jj] = quotient(t.v[i][j], u);
+        for (int jj = 0; jj < 4; ++jj) {
+          const int j = h * 4 + jj;
+          const int u = by_row ? i : (by_col ? j : 0);
+          q[jj] = qf(t.v[i][j], su[u], ru[u]);
+        }
+        uint32_t w = e4m3_pack2<false>(q[0], q[1], 0u);
+        packed[i][h] = e4m3_pack2<true>(q[2], q[3], w);
       }
-      uint32_t w = e4m3_pack2<false>(q[0], q[1], 0u);
-      packed[i][h] = e4m3_pack2<true>(q[2], q[3], w);
     }
-  }
+  };
+  if (wave_fast)
+    encode_all([](float x, float s_, float r_) { return fast_quotient(x, s_, r_); });
+  else
+    encode_all([](float x, float s_, float r_) { return slow_quotient(x, s_, r_); });
 
   if (!TRANS) {
     if (c < a.cols) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const int64_t r = r0 + rg * 8 + i;
+        const int64_t r = row0 + i;
         if (r < a.rows)
           *reinterpret_cast<uint2*>(a.codes + r * a.ldc + c) = make_uint2(packed[i][0], packed[i][1]);
       }
@@ -194,25 +259,19 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
 
   // scales of the block granularities (TENSOR / ROW / COL are finalized later)
   if (K == kBlock1x128) {
-    // output index (c0 / 128) * rows + r, the same for the transposed layout
-    if (cc < 8) {
-      float s = us[0].s;
-#pragma unroll
-      for (int i = 1; i < 8; ++i) s = (cc == i) ? us[i].s : s;
-      const int64_t r = r0 + rg * 8 + cc;
-      if (r < a.rows) a.scales[(int64_t)blockIdx.x * a.rows + r] = s;
-    }
+    // output index (c / 128) * rows + r, the same for the transposed layout;
+    // lane cc < 8 of a row group holds the scale of the thread's row cc
+    const int64_t r = row0 + cc;
+    if (cc < 8 && r < a.rows && c < a.cols) a.scales[(c >> 7) * a.rows + r] = mine.s;
   } else if (K == kBlock128x1) {
-    // output index (r0 / 128) * cols + c, the same for the transposed layout
-    if (rg == 0 && c < a.cols) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) a.scales[(int64_t)blockIdx.y * a.cols + c + j] = us[j].s;
-    }
+    // output index (r0 / 128) * cols + c, the same for the transposed layout;
+    // thread (rg < 8, cc) holds column 8 cc + rg's scale
+    const int64_t cj = c0 + cc * 8 + rg;
+    if (rg < 8 && cj < a.cols) a.scales[tr * a.cols + cj] = mine.s;
   } else if (K == kBlock128x128) {
     if (threadIdx.x == 0) {
-      const int64_t idx = TRANS ? (int64_t)blockIdx.x * gridDim.y + blockIdx.y
-                                : (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
-      a.scales[idx] = us[0].s;
+      const int64_t idx = TRANS ? tc * tiles_r + tr : tr * tiles_c + tc;
+      a.scales[idx] = mine.s;
     }
   }
 }
@@ -226,7 +285,7 @@ __global__ __launch_bounds__(kThreads) void amax_tile_kernel(QuantArgs a) {
   const int64_t r0 = (int64_t)blockIdx.y * kTile;
   const int64_t c0 = (int64_t)blockIdx.x * kTile;
   Tile t;
-  load_tile(a, r0, c0, t);
+  load_patch(a, r0 + rg * 8, c0 + cc * 8, t);
   unsigned int* bits = reinterpret_cast<unsigned int*>(a.scales);
   if (K == kPreRow) {
 #pragma unroll
@@ -268,7 +327,9 @@ __global__ void cast_f32_kernel(const float* x, int64_t n, float scale, uint8_t*
 
 template <int K, bool TRANS>
 hipError_t launch_tile(const QuantArgs& a, hipStream_t s) {
-  const dim3 grid((unsigned)((a.cols + kTile - 1) / kTile), (unsigned)((a.rows + kTile - 1) / kTile));
+  constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow);
+  constexpr int64_t tr = kWide ? kWideRows : kTile, tc = kWide ? kWideCols : kTile;
+  const dim3 grid((unsigned)((a.cols + tc - 1) / tc), (unsigned)((a.rows + tr - 1) / tr));
   quant_tile_kernel<K, TRANS><<<grid, kThreads, 0, s>>>(a);
   return hipGetLastError();
 }
