@@ -100,6 +100,44 @@ __device__ __noinline__ float slow_quotient(float x, float s, float r) {
   return quotient(x, UnitScale{s, r, s >= 0x1p-90f});
 }
 
+// Which of a thread's 8 x 8 elements share a unit: its rows, its columns, or
+// all of them.
+enum UnitMap { kUnitRow, kUnitCol, kUnitOne };
+
+// Codes of a thread's 8 x 8 patch, two E4M3 bytes per conversion: byte j of
+// packed[i][j / 4] is element (i, j), with the unit scales su (S) and ru
+// (1/S) indexed by row, by column, or [0].  The reciprocal-based quotient
+// holds for S >= 2^-90 (see quotient()); waves whose units all satisfy it
+// take the branch-free path.
+template <int MAP>
+__device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8], const float (&ru)[8],
+                                             uint32_t (&packed)[8][2]) {
+  bool fast = true;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) fast = fast && su[i] >= 0x1p-90f;
+  auto encode_all = [&](auto qf) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        float q[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          const int j = h * 4 + jj;
+          const int u = MAP == kUnitRow ? i : (MAP == kUnitCol ? j : 0);
+          q[jj] = qf(t.v[i][j], su[u], ru[u]);
+        }
+        uint32_t w = e4m3_pack2<false>(q[0], q[1], 0u);
+        packed[i][h] = e4m3_pack2<true>(q[2], q[3], w);
+      }
+    }
+  };
+  if (__all(fast))
+    encode_all([](float x, float s_, float r_) { return fast_quotient(x, s_, r_); });
+  else
+    encode_all([](float x, float s_, float r_) { return slow_quotient(x, s_, r_); });
+}
+
 template <int K, bool TRANS>
 __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   __shared__ float lds_red[4 * kTile];
@@ -187,36 +225,8 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
     }
   }
 
-  // The reciprocal-based quotient holds for S >= 2^-90 (see quotient());
-  // waves whose units all satisfy it take the branch-free path.
-  bool fast = true;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) fast = fast && su[i] >= 0x1p-90f;
-  const bool wave_fast = __all(fast);
-
-  // codes, two E4M3 bytes per conversion; q[i][j] -> byte j of row i
   uint32_t packed[8][2];
-  auto encode_all = [&](auto qf) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        float q[4];
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) {
-          const int j = h * 4 + jj;
-          const int u = by_row ? i : (by_col ? j : 0);
-          q[jj] = qf(t.v[i][j], su[u], ru[u]);
-        }
-        uint32_t w = e4m3_pack2<false>(q[0], q[1], 0u);
-        packed[i][h] = e4m3_pack2<true>(q[2], q[3], w);
-      }
-    }
-  };
-  if (wave_fast)
-    encode_all([](float x, float s_, float r_) { return fast_quotient(x, s_, r_); });
-  else
-    encode_all([](float x, float s_, float r_) { return slow_quotient(x, s_, r_); });
+  encode_patch<by_row ? kUnitRow : (by_col ? kUnitCol : kUnitOne)>(t, su, ru, packed);
 
   if (!TRANS) {
     if (c < a.cols) {
