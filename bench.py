@@ -30,11 +30,12 @@ WORKLOADS = {
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=50,
+                   help="untimed steps first (the clock settles over the first few dozen)")
     p.add_argument("--workload", default="8b_ffn_up_fwd_blockwise", choices=sorted(WORKLOADS))
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=256,
+    p.add_argument("--cpu-rows", type=int, default=4096,
                    help="rows of X the oracle processes for the CPU baseline")
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
                    help="after timing, run one plain device-to-device copy of this many "

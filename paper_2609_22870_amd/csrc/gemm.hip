@@ -31,6 +31,8 @@ namespace gemm_detail {
 
 typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 
 constexpr int kBK = 128;
 constexpr int kGroupM = 8;  // tile rows per group of the raster
@@ -561,11 +563,16 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     const uint4 v = *reinterpret_cast<const uint4*>(lds + mt * kRowBytes + ((c ^ (mt & 15)) << 4));
     uint16_t* dst = g.C + m * g.ldc + n;
     if (n + 8 <= g.N) {
+      // non-temporal: C is not read again here, and streaming it out keeps
+      // the last-level cache clean for the operands and for the kernels
+      // that follow (its write-back then overlaps this compute-bound kernel)
       if (g.c_aligned16) {
-        *reinterpret_cast<uint4*>(dst) = v;
+        const v4u vv = {v.x, v.y, v.z, v.w};
+        __builtin_nontemporal_store(vv, reinterpret_cast<v4u*>(dst));
       } else {
-        reinterpret_cast<uint2*>(dst)[0] = make_uint2(v.x, v.y);
-        reinterpret_cast<uint2*>(dst)[1] = make_uint2(v.z, v.w);
+        const v2u lo = {v.x, v.y}, hi = {v.z, v.w};
+        __builtin_nontemporal_store(lo, reinterpret_cast<v2u*>(dst));
+        __builtin_nontemporal_store(hi, reinterpret_cast<v2u*>(dst) + 1);
       }
     } else {
       const uint32_t w[4] = {v.x, v.y, v.z, v.w};
