@@ -360,20 +360,29 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     // before using them).  A bare barrier: __syncthreads() would add a
     // release fence (a wait the loads above already made).
     asm volatile("s_barrier" ::: "memory");
-    // the vector-memory slots of strip I
+    // Vector-memory slot Q of strip I (I = -1: the ones right after the
+    // barrier).  Within a strip each goes out right after one of the
+    // strip's MFMAs, so a stall on the queue overlaps that MFMA.
+    auto issue_one = [&](auto ic, auto qc) {
+      constexpr int I = decltype(ic)::value, Q = decltype(qc)::value;
+      constexpr int S = I < 0 ? Q : kPre + I * kPerStrip + Q;
+      if constexpr (kMore && S < kSlots && (I < 0 ? Q < kPre : Q < kPerStrip)) {
+        if constexpr (S < kS0)
+          load_scales(kt + 1);
+        else if constexpr (S - kS0 < kPerA)
+          ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>((kt + 1) * kBK, nxt, wave);
+        else
+          ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>((kt + 1) * kBK, nxt + kTileA, wave);
+      }
+    };
     auto issue_strip = [&](auto ic) {
-      constexpr int I = decltype(ic)::value;
-      if constexpr (kMore) static_for<kSlots>([&](auto sc) {
-        constexpr int S = decltype(sc)::value;
-        if constexpr (I < 0 ? S < kPre : (S >= kPre + I * kPerStrip && S < kPre + (I + 1) * kPerStrip)) {
-          if constexpr (S < kS0)
-            load_scales(kt + 1);
-          else if constexpr (S - kS0 < kPerA)
-            ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>((kt + 1) * kBK, nxt, wave);
-          else
-            ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>((kt + 1) * kBK, nxt + kTileA, wave);
-        }
-      });
+      static_for<(kPre > kPerStrip ? kPre : kPerStrip)>([&](auto qc) { issue_one(ic, qc); });
+    };
+    // MFMA j of a strip, then its vector-memory slot
+    auto after_mfma = [&](auto ic, auto jc) {
+      sched_fence();
+      issue_one(ic, jc);
+      sched_fence();
     };
 
     // Fragment reads of the first two strips: A strip 0, the B fragments,
@@ -438,10 +447,8 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
           constexpr int j = decltype(jc)::value;
           if constexpr (i == 0) wait_b(jc);
           acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
-          if constexpr (i == 0) sched_fence();
+          after_mfma(ic, jc);
         });
-        issue_strip(ic);
-        sched_fence();
         v8i af_after = af_next;
         if constexpr (i + 2 < TI) {
           if constexpr (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
@@ -485,12 +492,16 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
           if constexpr (i > 0) order_after(af_next, acc[i - 1]);
           // af_next was read before the scales (strip 0) or a strip ago
           lds_wait<kAfter + (i == 0 ? kScaleReads : 0)>(af_next);
-#pragma unroll
-          for (int j = 0; j < TJ; ++j) p_next[j] = mfma_16x16x128(bf[j], af_next, zero);
+          static_for<TJ>([&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            p_next[j] = mfma_16x16x128(bf[j], af_next, zero);
+            after_mfma(ic, jc);
+          });
+        } else {
+          sched_fence();
+          issue_strip(ic);
+          sched_fence();
         }
-        sched_fence();
-        issue_strip(ic);
-        sched_fence();
         if constexpr (i == 0) {
           asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(kAfter));
           scales_ready();
