@@ -208,6 +208,12 @@ __device__ __forceinline__ void lds_wait2(v8i& f, v8i& h) {
 }
 
 __device__ __forceinline__ void wait_vmem_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// at most N vector-memory instructions of this wave still in flight
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -255,9 +261,15 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   constexpr int kScaleA = kBlockScaled ? BM * 4 : 0;
   constexpr int kScaleB = PAIR == kPairBlockK ? BN * 4 : (PAIR == kPairBlock ? 256 : 0);
   constexpr int kScaleStage = kScaleA + kScaleB;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStage + 2 * kScaleStage + kWaves * 256];
-  uint8_t* const scale_lds = lds + 2 * kStage;
-  uint8_t* const dummy_lds = lds + 2 * kStage + 2 * kScaleStage;  // 256 bytes per wave
+  // LDS ring of kStages operand stages (and their scale vectors): the loads
+  // of stage kt + kStages - 1 go out during step kt.  The 256 x 256 tile
+  // fits two 64 KB stages; 128 x 128 keeps two (more would cost it its
+  // second workgroup per CU); the 64 x 64 tile of skinny problems, whose
+  // steps are short next to the load latency, keeps four.
+  constexpr int kStages = BM >= 128 ? 2 : 4;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStage + kStages * kScaleStage + kWaves * 256];
+  uint8_t* const scale_lds = lds + kStages * kStage;
+  uint8_t* const dummy_lds = lds + kStages * kStage + kStages * kScaleStage;  // 256 bytes per wave
 
   int tm, tn;
   tile_coords<BM, BN>(g.M, g.N, tm, tn);
@@ -301,7 +313,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     q_dst = kScaleA + (wave - kQA) * 256;
     if (PAIR == kPairBlock) {
       // the tile's BN / 128 weight blocks, each with K / 128 scales
-      q_voff = lane < BN / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
+      q_voff = lane < (BN + 127) / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
       q_ld = 4;
     } else {
       q_voff = ((wave - kQA) * 64 + lane) * 4;
@@ -312,19 +324,23 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   q_dst = uniform(q_dst);
   q_ld = uniform(q_ld);
   q_base = uniform(q_base);
-  // LDS destination per stage (0, 1) of this wave's instruction
-  uint8_t* const q_to0 = wave < kQ ? scale_lds + q_dst : dummy_lds + wave * 256;
-  uint8_t* const q_to1 = wave < kQ ? scale_lds + kScaleStage + q_dst : dummy_lds + wave * 256;
-  auto load_scales = [&](int kt) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_void*)(kt & 1 ? q_to1 : q_to0), 4, q_voff,
+  // LDS destination of this wave's instruction: stage st's scale vectors
+  uint8_t* const q_to = wave < kQ ? scale_lds + q_dst : dummy_lds + wave * 256;
+  const int q_stride = uniform(wave < kQ ? kScaleStage : 0);
+  auto load_scales = [&](int kt, int st) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_void*)(q_to + st * q_stride), 4, q_voff,
                                              q_base + kt * q_ld, 0, 0);
   };
 
   const TileLoader<BM, kWaves> ldA(g.A, g.lda, m0, g.M, wave);
   const TileLoader<BN, kWaves> ldB(g.B, g.ldb, n0, g.N, wave);
-  if constexpr (kBlockScaled) load_scales(0);
-  ldA.load(0, lds, wave);
-  ldB.load(0, lds + kTileA, wave);
+  // prologue: stages 0 .. kStages - 2 (each wave issues kSlots loads per
+  // stage, with the scale slot first)
+  for (int st = 0; st < kStages - 1 && st < KT; ++st) {
+    if constexpr (kBlockScaled) load_scales(st, st);
+    ldA.load(st * kBK, lds + st * kStage, wave);
+    ldB.load(st * kBK, lds + st * kStage + kTileA, wave);
+  }
 
   // a VALU result computed from the last MFMA output of the previous step
   float done = 0.0f;
@@ -347,18 +363,27 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   constexpr int kScaleReads = PAIR == kPairBlock ? TI + 1 : (PAIR == kPairBlockK ? TI + TJ : 0);
   static_assert(kScaleReads + 2 <= 15, "outstanding LDS reads must fit the lgkm counter");
 
-  // One K step; kMore: the loads of stage kt+1 go out during it (all but
-  // the last step, which is peeled so that no step carries a branch).
+  // One K step; kMore: the loads of stage kt + kStages - 1 go out during
+  // it (all but the last kStages - 1 steps, which run without, so that no
+  // step carries a branch).
   auto step = [&](const int kt, auto more_c) __attribute__((always_inline)) {
     constexpr bool kMore = decltype(more_c)::value;
-    uint8_t* cur = lds + (kt & 1) * kStage;
-    uint8_t* cur_scales = scale_lds + (kt & 1) * kScaleStage;
-    uint8_t* nxt = lds + ((kt + 1) & 1) * kStage;
-    wait_vmem_all();
+    const int cur_st = kt % kStages, nxt_st = (kt + kStages - 1) % kStages;
+    uint8_t* cur = lds + cur_st * kStage;
+    uint8_t* cur_scales = scale_lds + cur_st * kScaleStage;
+    uint8_t* nxt = lds + nxt_st * kStage;
+    const int k_nxt = (kt + kStages - 1) * kBK;
+    // this wave's loads of stage kt have landed: only those of the later
+    // stages (kSlots each) may still be in flight
+    if constexpr (kMore)
+      wait_vmem<(kStages - 2) * kSlots>();
+    else
+      wait_vmem<0>();
     // Tile kt and its scales are in LDS for every wave (each waited for its
-    // own loads) and stage kt+1 is free (each waited for its LDS reads
-    // before using them).  A bare barrier: __syncthreads() would add a
-    // release fence (a wait the loads above already made).
+    // own loads) and the stage the loads of this step overwrite, kt - 1's,
+    // is free (each wave waited for its LDS reads before using them).  A
+    // bare barrier: __syncthreads() would add a release fence waiting for
+    // every load in flight.
     asm volatile("s_barrier" ::: "memory");
     // Vector-memory slot Q of strip I (I = -1: the ones right after the
     // barrier).  Within a strip each goes out right after one of the
@@ -368,20 +393,25 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       constexpr int S = I < 0 ? Q : kPre + I * kPerStrip + Q;
       if constexpr (kMore && S < kSlots && (I < 0 ? Q < kPre : Q < kPerStrip)) {
         if constexpr (S < kS0)
-          load_scales(kt + 1);
+          load_scales(kt + kStages - 1, nxt_st);
         else if constexpr (S - kS0 < kPerA)
-          ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>((kt + 1) * kBK, nxt, wave);
+          ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>(k_nxt, nxt, wave);
         else
-          ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>((kt + 1) * kBK, nxt + kTileA, wave);
+          ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>(k_nxt, nxt + kTileA, wave);
       }
     };
     auto issue_strip = [&](auto ic) {
       static_for<(kPre > kPerStrip ? kPre : kPerStrip)>([&](auto qc) { issue_one(ic, qc); });
     };
-    // MFMA j of a strip, then its vector-memory slot
+    // after MFMA j of a strip: its vector-memory slot (after the strip's
+    // last MFMA, any slots beyond the strip's MFMA count too)
     auto after_mfma = [&](auto ic, auto jc) {
+      constexpr int j = decltype(jc)::value;
       sched_fence();
       issue_one(ic, jc);
+      if constexpr (j == TJ - 1)
+        static_for<(kPerStrip > TJ ? kPerStrip - TJ : 0)>(
+            [&](auto qc) { issue_one(ic, std::integral_constant<int, TJ + decltype(qc)::value>{}); });
       sched_fence();
     };
 
@@ -525,8 +555,9 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       done = acc[TI - 1][TJ - 1][3];
     }
   };
-  for (int kt = 0; kt + 1 < KT; ++kt) step(kt, std::true_type{});
-  step(KT - 1, std::false_type{});
+  int kt = 0;
+  for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{});
+  for (; kt < KT; ++kt) step(kt, std::false_type{});
 
   // Epilogue: whole-K scales for tensor / row pairs, bf16 RNE, then the
   // tile goes through LDS (the operand stages are free now) so that global
@@ -534,13 +565,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // tile holds BN bf16; its 16-byte chunk c sits at chunk c ^ (m & 15), which
   // keeps both the 8-byte writes (16 rows, same columns) and the 16-byte
   // reads (one row) free of bank conflicts.
-  static_assert(BM * BN * 2 <= 2 * kStage, "C tile must fit in the LDS stages");
+  static_assert(BM * BN * 2 <= kStages * kStage, "C tile must fit in the LDS stages");
   const int voff_m = (lane & 15) * 4, voff_n = (lane >> 4) * 16;
   float st = 1.0f;
   if (PAIR == kPairTensor) st = load_f32(rsA, 0, 0) * load_f32(rsB, 0, 0);
   wait_vmem_all();  // no load may still be writing LDS
   __syncthreads();  // every wave is done with the operand stages
   constexpr int kRowBytes = BN * 2;
+  constexpr int kChunkMask = kRowBytes / 16 < 16 ? kRowBytes / 16 - 1 : 15;  // the swizzle stays in the row
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
     const int mt = wm + i * 16 + (lane & 15);  // row within the tile
@@ -557,7 +589,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
         h[r] = bf16_rne(v);
       }
       const int chunk = (nt * 2) >> 4, half = ((nt * 2) >> 3) & 1;
-      *reinterpret_cast<uint2*>(lds + mt * kRowBytes + ((chunk ^ (mt & 15)) << 4) + half * 8) =
+      *reinterpret_cast<uint2*>(lds + mt * kRowBytes + ((chunk ^ (mt & kChunkMask)) << 4) + half * 8) =
           make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
     }
   }
@@ -571,7 +603,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   for (int mt = threadIdx.x / kChunksPerRow; mt < BM; mt += kRowsPerPass) {
     const int64_t m = m0 + mt;
     if (m >= g.M || n >= g.N) continue;
-    const uint4 v = *reinterpret_cast<const uint4*>(lds + mt * kRowBytes + ((c ^ (mt & 15)) << 4));
+    const uint4 v = *reinterpret_cast<const uint4*>(lds + mt * kRowBytes + ((c ^ (mt & kChunkMask)) << 4));
     uint16_t* dst = g.C + m * g.ldc + n;
     if (n + 8 <= g.N) {
       // non-temporal: C is not read again here, and streaming it out keeps
@@ -602,14 +634,18 @@ hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
 }
 
 // 256 x 256 tiles (8 waves of 128 x 64) when they fill the chip at least
-// twice over; 128 x 128 tiles (4 waves of 64 x 64) otherwise.
+// twice over; else 128 x 128 tiles (4 waves of 64 x 64) when they fill it
+// once; else 64 x 64 tiles (4 waves of 32 x 32), for skinny problems such as
+// a decode step, whose time goes into streaming the weights.
 template <int PAIR>
 hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  const int64_t mid_tiles = ((g.M + 127) / 128) * ((g.N + 127) / 128);
   if constexpr (PAIR != kPairBlockK) {
     if (big_tiles >= 512) return launch_tiles<PAIR, 256, 256, 128, 64>(g, s);
   }
-  return launch_tiles<PAIR, 128, 128, 64, 64>(g, s);
+  if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64>(g, s);
+  return launch_tiles<PAIR, 64, 64, 32, 32>(g, s);
 }
 
 // The kernels address operands with 32-bit offsets: split the problem into
@@ -661,6 +697,10 @@ FP8Q_GEMM_KERNEL(kPairRow, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairBlock, 256, 256, 128, 64)
 FP8Q_GEMM_KERNEL(kPairBlock, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairBlockK, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL(kPairTensor, 64, 64, 32, 32)
+FP8Q_GEMM_KERNEL(kPairRow, 64, 64, 32, 32)
+FP8Q_GEMM_KERNEL(kPairBlock, 64, 64, 32, 32)
+FP8Q_GEMM_KERNEL(kPairBlockK, 64, 64, 32, 32)
 #undef FP8Q_GEMM_KERNEL
 
 }  // namespace gemm_detail
