@@ -21,16 +21,31 @@ FLAGS = [
 ]
 
 
+def check_no_scratch(src, remarks):
+    """The GEMM kernels read LDS with inline asm whose results are only valid
+    after an explicit wait; a register spill could copy such a value early.
+    Refuse a build in which any GEMM kernel uses scratch memory."""
+    name = None
+    for line in remarks.splitlines():
+        if "Function Name:" in line:
+            name = line.split("Function Name:")[1].split()[0]
+        elif "ScratchSize [bytes/lane]:" in line and name and "gemm_kernel" in name:
+            size = int(line.split("ScratchSize [bytes/lane]:")[1].split()[0])
+            if size != 0:
+                raise RuntimeError("%s: %s spills to scratch (%d bytes per lane)" % (src, name, size))
+
+
 def build():
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
 
     def compile_one(src):
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        cmd = [HIPCC] + FLAGS + ["-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC] + FLAGS + ["-Rpass-analysis=kernel-resource-usage", "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError("hipcc failed for %s:\n%s" % (src, r.stderr))
+        check_no_scratch(src, r.stderr)
         return obj
 
     with ThreadPoolExecutor(len(SOURCES)) as ex:

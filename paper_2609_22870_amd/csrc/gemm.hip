@@ -231,10 +231,9 @@ __device__ __forceinline__ void order_after(v8i& next, v4f (&done)[TJ]) {
 // the raster walks kGroupM tile rows at a time so that consecutive tiles
 // reuse A rows and B rows.
 template <int BM, int BN>
-__device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int& tm, int& tn) {
+__device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int b, int& tm, int& tn) {
   const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
   const int total = tiles_m * tiles_n;
-  const int b = blockIdx.x;
   const int xcd = b & 7, per = total >> 3, extra = total & 7;
   const int id = xcd * per + (xcd < extra ? xcd : extra) + (b >> 3);
   const int per_group = kGroupM * tiles_n;
@@ -272,7 +271,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   uint8_t* const dummy_lds = lds + kStages * kStage + kStages * kScaleStage;  // 256 bytes per wave
 
   int tm, tn;
-  tile_coords<BM, BN>(g.M, g.N, tm, tn);
+  tile_coords<BM, BN>(g.M, g.N, blockIdx.x, tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
@@ -304,26 +303,29 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const bool q_is_a = wave < kQA;
   const __amdgpu_buffer_rsrc_t rs_q = q_is_a ? rsA : rsB;
   int q_dst = 0, q_voff = 0x7fffffff, q_ld = 0, q_base = 0;
-  if (wave < kQA) {
-    q_dst = wave * 256;
-    q_voff = (wave * 64 + lane) * 4;
-    q_ld = (int)g.sa_ld * 4;
-    q_base = (int)m0 * 4;
-  } else if (wave < kQ) {
-    q_dst = kScaleA + (wave - kQA) * 256;
-    if (PAIR == kPairBlock) {
-      // the tile's BN / 128 weight blocks, each with K / 128 scales
-      q_voff = lane < (BN + 127) / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
-      q_ld = 4;
-    } else {
-      q_voff = ((wave - kQA) * 64 + lane) * 4;
-      q_ld = (int)g.sb_ld * 4;
-      q_base = (int)n0 * 4;
+  auto scale_offsets = [&]() {  // of the tile at (m0, n0)
+    if (wave < kQA) {
+      q_dst = wave * 256;
+      q_voff = (wave * 64 + lane) * 4;
+      q_ld = (int)g.sa_ld * 4;
+      q_base = (int)m0 * 4;
+    } else if (wave < kQ) {
+      q_dst = kScaleA + (wave - kQA) * 256;
+      if (PAIR == kPairBlock) {
+        // the tile's BN / 128 weight blocks, each with K / 128 scales
+        q_voff = lane < (BN + 127) / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
+        q_ld = 4;
+      } else {
+        q_voff = ((wave - kQA) * 64 + lane) * 4;
+        q_ld = (int)g.sb_ld * 4;
+        q_base = (int)n0 * 4;
+      }
     }
-  }
-  q_dst = uniform(q_dst);
-  q_ld = uniform(q_ld);
-  q_base = uniform(q_base);
+    q_dst = uniform(q_dst);
+    q_ld = uniform(q_ld);
+    q_base = uniform(q_base);
+  };
+  scale_offsets();
   // LDS destination of this wave's instruction: stage st's scale vectors
   uint8_t* const q_to = wave < kQ ? scale_lds + q_dst : dummy_lds + wave * 256;
   const int q_stride = uniform(wave < kQ ? kScaleStage : 0);
@@ -336,11 +338,22 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const TileLoader<BN, kWaves> ldB(g.B, g.ldb, n0, g.N, wave);
   // prologue: stages 0 .. kStages - 2 (each wave issues kSlots loads per
   // stage, with the scale slot first)
-  for (int st = 0; st < kStages - 1 && st < KT; ++st) {
-    if constexpr (kBlockScaled) load_scales(st, st);
-    ldA.load(st * kBK, lds + st * kStage, wave);
-    ldB.load(st * kBK, lds + st * kStage + kTileA, wave);
-  }
+  auto prologue = [&]() {
+    if constexpr (kStages == 2) {
+      // stage 0, then stage 1's B tile (see the schedule below)
+      if constexpr (kBlockScaled) load_scales(0, 0);
+      ldA.load(0, lds, wave);
+      ldB.load(0, lds + kTileA, wave);
+      if (KT > 1) ldB.load(kBK, lds + kStage + kTileA, wave);
+    } else {
+      for (int st = 0; st < kStages - 1 && st < KT; ++st) {
+        if constexpr (kBlockScaled) load_scales(st, st);
+        ldA.load(st * kBK, lds + st * kStage, wave);
+        ldB.load(st * kBK, lds + st * kStage + kTileA, wave);
+      }
+    }
+  };
+  prologue();
 
   // a VALU result computed from the last MFMA output of the previous step
   float done = 0.0f;
@@ -358,6 +371,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // first fragments; the rest kPerStrip per strip
   constexpr int kPre = TI >= 8 ? 2 : 0;
   constexpr int kPerStrip = (kSlots - kPre + TI - 1) / TI > 2 ? (kSlots - kPre + TI - 1) / TI : 2;
+  // With two stages the B tile is loaded two steps ahead.  A wave reads its
+  // B fragments at the start of a step, so after a second barrier (once
+  // every wave holds them, after the first strip's MFMAs) the B half of the
+  // current stage is free: the next-but-one stage's B tile goes there during
+  // the second half of the step, while the next stage's scales and A tile go
+  // out in the first half.  The post-barrier burst halves and the B loads
+  // get one and a half steps to land.
+  constexpr bool kSplitB = kStages == 2;
+  constexpr int kNA = kS0 + kPerA;                                   // A-part slots
+  constexpr int kPerStripA = (kNA - kPre + TI / 2 - 1) / (TI / 2) > 1 ? (kNA - kPre + TI / 2 - 1) / (TI / 2) : 1;
+  constexpr int kPerStripB = (kPerB + TI / 2 - 1) / (TI / 2);        // strips TI/2 .. TI-1
   static_assert(kQ <= kWaves, "at most one scale-vector load per wave and step");
   // LDS reads of the step's scales, issued after the first strip's MFMAs
   constexpr int kScaleReads = PAIR == kPairBlock ? TI + 1 : (PAIR == kPairBlockK ? TI + TJ : 0);
@@ -366,19 +390,31 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // One K step; kMore: the loads of stage kt + kStages - 1 go out during
   // it (all but the last kStages - 1 steps, which run without, so that no
   // step carries a branch).
-  auto step = [&](const int kt, auto more_c) __attribute__((always_inline)) {
+  // kMore: with two stages, the next stage's A tile and scales go out
+  // (kMoreB: and the next-but-one's B tile); with more stages, all loads
+  // of stage kt + kStages - 1.
+  auto step = [&](const int kt, auto more_c, auto more_b_c) __attribute__((always_inline)) {
     constexpr bool kMore = decltype(more_c)::value;
+    constexpr bool kMoreB = decltype(more_b_c)::value;
     const int cur_st = kt % kStages, nxt_st = (kt + kStages - 1) % kStages;
     uint8_t* cur = lds + cur_st * kStage;
     uint8_t* cur_scales = scale_lds + cur_st * kScaleStage;
     uint8_t* nxt = lds + nxt_st * kStage;
     const int k_nxt = (kt + kStages - 1) * kBK;
-    // this wave's loads of stage kt have landed: only those of the later
-    // stages (kSlots each) may still be in flight
-    if constexpr (kMore)
-      wait_vmem<(kStages - 2) * kSlots>();
-    else
-      wait_vmem<0>();
+    const int k_b2 = (kt + 2 < KT ? kt + 2 : KT - 1) * kBK;  // two-stage B tile
+    // this wave's loads of stage kt have landed: only those of later stages
+    // may still be in flight (two stages: stage kt+1's B tile, issued last)
+    if constexpr (kSplitB) {
+      if constexpr (kMore)
+        wait_vmem<kPerB>();
+      else
+        wait_vmem<0>();
+    } else {
+      if constexpr (kMore)
+        wait_vmem<(kStages - 2) * kSlots>();
+      else
+        wait_vmem<0>();
+    }
     // Tile kt and its scales are in LDS for every wave (each waited for its
     // own loads) and the stage the loads of this step overwrite, kt - 1's,
     // is free (each wave waited for its LDS reads before using them).  A
@@ -388,20 +424,48 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     // Vector-memory slot Q of strip I (I = -1: the ones right after the
     // barrier).  Within a strip each goes out right after one of the
     // strip's MFMAs, so a stall on the queue overlaps that MFMA.
+    auto issue_slot = [&](auto sc, auto kb_c) {  // slot S; kb_c: B tile two stages ahead
+      constexpr int S = decltype(sc)::value;
+      if constexpr (S < kS0)
+        load_scales(kt + kStages - 1, nxt_st);
+      else if constexpr (S - kS0 < kPerA)
+        ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>(k_nxt, nxt, wave);
+      else if constexpr (decltype(kb_c)::value)
+        ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>(k_b2, cur + kTileA, wave);
+      else
+        ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>(k_nxt, nxt + kTileA, wave);
+    };
+    constexpr int kQMax = kSplitB ? (kPre > kPerStripA + kPerStripB ? kPre : kPerStripA + kPerStripB)
+                                  : (kPre > kPerStrip ? kPre : kPerStrip);
     auto issue_one = [&](auto ic, auto qc) {
       constexpr int I = decltype(ic)::value, Q = decltype(qc)::value;
-      constexpr int S = I < 0 ? Q : kPre + I * kPerStrip + Q;
-      if constexpr (kMore && S < kSlots && (I < 0 ? Q < kPre : Q < kPerStrip)) {
-        if constexpr (S < kS0)
-          load_scales(kt + kStages - 1, nxt_st);
-        else if constexpr (S - kS0 < kPerA)
-          ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>(k_nxt, nxt, wave);
-        else
-          ldB.template load_group<(S - kS0 >= kPerA ? S - kS0 - kPerA : 0)>(k_nxt, nxt + kTileA, wave);
+      if constexpr (kSplitB) {
+        // A part: kPre after the barrier, then kPerStripA per strip; B part:
+        // kPerStripB per strip from strip TI/2 on
+        constexpr int SA = I < 0 ? Q : kPre + I * kPerStripA + Q;
+        constexpr bool a_here = (I < 0 ? Q < kPre : Q < kPerStripA) && SA < kNA;
+        constexpr int QB = I < 0 ? -1 : (SA < kNA ? Q - kPerStripA : Q - kPerStripA);
+        constexpr int SB = kNA + (I - TI / 2) * kPerStripB + QB;
+        constexpr bool b_here = I >= TI / 2 && QB >= 0 && QB < kPerStripB && SB < kSlots;
+        if constexpr (kMore && a_here) issue_slot(std::integral_constant<int, SA>{}, std::false_type{});
+        if constexpr (kMoreB && b_here) issue_slot(std::integral_constant<int, SB>{}, std::true_type{});
+      } else {
+        constexpr int S = I < 0 ? Q : kPre + I * kPerStrip + Q;
+        if constexpr (kMore && S < kSlots && (I < 0 ? Q < kPre : Q < kPerStrip))
+          issue_slot(std::integral_constant<int, S>{}, std::false_type{});
       }
     };
     auto issue_strip = [&](auto ic) {
-      static_for<(kPre > kPerStrip ? kPre : kPerStrip)>([&](auto qc) { issue_one(ic, qc); });
+      static_for<kQMax>([&](auto qc) { issue_one(ic, qc); });
+    };
+    // the second barrier of a two-stage step (after the first strip's
+    // MFMAs: every wave holds its B fragments)
+    auto mid_barrier = [&]() {
+      if constexpr (kSplitB && kMoreB) {
+        sched_fence();
+        asm volatile("s_barrier" ::: "memory");
+        sched_fence();
+      }
     };
     // after MFMA j of a strip: its vector-memory slot (after the strip's
     // last MFMA, any slots beyond the strip's MFMA count too)
@@ -410,7 +474,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       sched_fence();
       issue_one(ic, jc);
       if constexpr (j == TJ - 1)
-        static_for<(kPerStrip > TJ ? kPerStrip - TJ : 0)>(
+        static_for<(kQMax > TJ ? kQMax - TJ : 0)>(
             [&](auto qc) { issue_one(ic, std::integral_constant<int, TJ + decltype(qc)::value>{}); });
       sched_fence();
     };
@@ -479,6 +543,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
           acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
           after_mfma(ic, jc);
         });
+        if constexpr (i == 0) mid_barrier();
         v8i af_after = af_next;
         if constexpr (i + 2 < TI) {
           if constexpr (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
@@ -511,6 +576,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
         p[j] = mfma_16x16x128(bf[j], af, zero);
         sched_fence();
       });
+      mid_barrier();
       read_scales();
       static_for<TI>([&](auto ic) {
         constexpr int i = decltype(ic)::value;
@@ -555,9 +621,21 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       done = acc[TI - 1][TJ - 1][3];
     }
   };
-  int kt = 0;
-  for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{});
-  for (; kt < KT; ++kt) step(kt, std::false_type{});
+  auto all_steps = [&]() {
+    int kt = 0;
+    if constexpr (kSplitB) {
+      // (the B load of step KT-2 re-reads stage KT-1's B tile into a buffer
+      // nothing reads again: a third copy of the step body, without it,
+      // would push the kernel past its registers)
+      for (; kt + 1 < KT; ++kt) step(kt, std::true_type{}, std::true_type{});
+      step(kt, std::false_type{}, std::false_type{});
+    } else {
+      for (; kt + kStages - 1 < KT; ++kt) step(kt, std::true_type{}, std::false_type{});
+      for (; kt < KT; ++kt) step(kt, std::false_type{}, std::false_type{});
+    }
+  };
+
+  all_steps();
 
   // Epilogue: whole-K scales for tensor / row pairs, bf16 RNE, then the
   // tile goes through LDS (the operand stages are free now) so that global
@@ -652,11 +730,15 @@ hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
 // sub-GEMMs whose A and B row ranges each span less than 4 GiB.
 template <int PAIR>
 hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
-  // 32-bit offsets: each sub-problem's A rows and B rows span < 2 GiB, and
-  // row / column indices stay below 2^31 / 4
+  // 32-bit offsets: each sub-problem's A rows, B rows and C rows span
+  // < 2 GiB, and row / column indices stay below 2^31 / 4
   const int64_t lim = (int64_t)1 << 31;
   int64_t mstep = g.M, nstep = g.N;
   if (g.M * g.lda >= lim) mstep = ((lim - 1) / g.lda) / 256 * 256;
+  if (g.M * g.ldc * 2 >= lim) {
+    const int64_t cstep = ((lim - 1) / (2 * g.ldc)) / 256 * 256;
+    if (cstep < mstep) mstep = cstep;
+  }
   if (g.N * g.ldb >= lim) nstep = ((lim - 1) / g.ldb) / 256 * 256;
   if (mstep > ((int64_t)1 << 28)) mstep = (int64_t)1 << 28;
   if (nstep > ((int64_t)1 << 28)) nstep = (int64_t)1 << 28;

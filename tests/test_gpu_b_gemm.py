@@ -187,6 +187,25 @@ def test_determinism_and_guard_bands():
     assert torch.all(buf[:4096] == -12345.0) and torch.all(buf[4096 + M * N:] == -12345.0)
 
 
+def test_many_tiles_ragged_blockwise():
+    """Blockwise pair on enough 256 x 256 tiles that each workgroup of the
+    large-problem kernel takes several in turn (3185 tiles), with a ragged
+    last tile row (M = 64 * 256 + 160) and a last tile column only half
+    inside N (N = 97 * 128); the sampled rows include the last band."""
+    M, K, N = 16384 + 160, 256, 97 * 128
+    a = synth.activations(M, K, seed=141, outlier_seed=142, device=DEV)
+    b = synth.weights(N, K, seed=143, device=DEV)
+    rows = np.unique(np.concatenate([_par.sample_rows(M), np.arange(M - 40, M)]))
+    run_pair(a, b, fp8q.BLOCK_1x128, fp8q.BLOCK_128x128, rows=rows, label="many tiles ragged")
+    # columns past N stay untouched in a padded output
+    A, sA = fp8q.quantize(a, fp8q.BLOCK_1x128)
+    B, sB = fp8q.quantize(b, fp8q.BLOCK_128x128)
+    buf = torch.full((M, N + 64), -7.0, dtype=torch.bfloat16, device=DEV)
+    fp8q.gemm(A, sA, fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128, out=buf[:, :N])
+    torch.cuda.synchronize()
+    assert torch.all(buf[:, N:] == -7.0)
+
+
 # ---- the named workloads at full size, sampled rows (2 per 128-row band)
 
 def test_full_8b_ffn_up_blockwise():
