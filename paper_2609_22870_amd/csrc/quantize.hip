@@ -318,6 +318,71 @@ __global__ __launch_bounds__(kThreads) void amax_tile_kernel(QuantArgs a) {
   }
 }
 
+// ROW units without transposition, in one pass over memory: a wave takes
+// one row at a time.  Lane l holds the 16-byte pieces l, l + 64, ... of a
+// 4096-element chunk of the row, so each load instruction reads 1 KB of it,
+// and the row's amax is a wave reduction.  A row of more than 4096 elements
+// is walked twice, the second time out of L2: for its amax, then for its
+// codes.
+constexpr int kRowChunk = 4096;
+constexpr int kRowWaves = 4;
+
+__device__ __forceinline__ void load_row_chunk(const QuantArgs& a, const uint16_t* xr, int64_t c0, Tile& t) {
+  const int lane = threadIdx.x & 63;
+  uint4 w[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int64_t c = c0 + q * 512 + lane * 8;
+    w[q] = make_uint4(0u, 0u, 0u, 0u);
+    if (c < a.cols) w[q] = *reinterpret_cast<const uint4*>(xr + c);
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    t.v[q][0] = bf16_lo(w[q].x);
+    t.v[q][1] = bf16_hi(w[q].x);
+    t.v[q][2] = bf16_lo(w[q].y);
+    t.v[q][3] = bf16_hi(w[q].y);
+    t.v[q][4] = bf16_lo(w[q].z);
+    t.v[q][5] = bf16_hi(w[q].z);
+    t.v[q][6] = bf16_lo(w[q].w);
+    t.v[q][7] = bf16_hi(w[q].w);
+  }
+}
+
+__global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) {
+  const int lane = threadIdx.x & 63;
+  const bool one_chunk = a.cols <= kRowChunk;
+  const int64_t stride = (int64_t)gridDim.x * kRowWaves;
+  for (int64_t r = (int64_t)blockIdx.x * kRowWaves + (threadIdx.x >> 6); r < a.rows; r += stride) {
+    const uint16_t* xr = a.x + r * a.ldx;
+    Tile t;
+    float m = 0.0f;
+    for (int64_t c0 = 0; c0 < a.cols; c0 += kRowChunk) {
+      load_row_chunk(a, xr, c0, t);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) m = fmaxf(m, row_partial_max(t, q));
+    }
+    const UnitScale u = unit_scale(wave_max(m));
+    float su[8], ru[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      su[i] = u.s;
+      ru[i] = u.r;
+    }
+    for (int64_t c0 = 0; c0 < a.cols; c0 += kRowChunk) {
+      if (!one_chunk) load_row_chunk(a, xr, c0, t);
+      uint32_t packed[8][2];
+      encode_patch<kUnitOne>(t, su, ru, packed);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int64_t c = c0 + q * 512 + lane * 8;
+        if (c < a.cols) *reinterpret_cast<uint2*>(a.codes + r * a.ldc + c) = make_uint2(packed[q][0], packed[q][1]);
+      }
+    }
+    if (lane == 0) a.scales[r] = u.s;
+  }
+}
+
 __global__ void fill_zero_kernel(float* p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0.0f;
@@ -369,7 +434,12 @@ hipError_t launch_quantize(const QuantArgs& a, int granularity, bool trans, int6
     case 4: return trans ? launch_tile<kBlock128x1, true>(a, s) : launch_tile<kBlock128x1, false>(a, s);
     case 5: return trans ? launch_tile<kBlock128x128, true>(a, s) : launch_tile<kBlock128x128, false>(a, s);
     case 0: return launch_two_pass<kPreTensor>(a, trans, nscales, s);
-    case 1: return launch_two_pass<kPreRow>(a, trans, nscales, s);
+    case 1: {
+      if (trans) return launch_two_pass<kPreRow>(a, trans, nscales, s);
+      const int64_t blocks = (a.rows + kRowWaves - 1) / kRowWaves;
+      quant_row_kernel<<<(unsigned)(blocks < 16384 ? blocks : 16384), kRowWaves * 64, 0, s>>>(a);
+      return hipGetLastError();
+    }
     case 2: return launch_two_pass<kPreCol>(a, trans, nscales, s);
     default: return hipErrorInvalidValue;
   }

@@ -50,6 +50,21 @@ def test_single_row_and_narrow(g):
           label="narrow")
 
 
+@pytest.mark.parametrize("cols", [4096, 4112, 12304])
+def test_long_rows(cols):
+    """Row units across one or several 4096-element chunks of a row, the
+    last chunk ragged (4112 = 4096 + 16, 12304 = 3 * 4096 + 16), read
+    through a padded leading dimension."""
+    x = synth.activations(70, cols, seed=31, outlier_seed=32)
+    xd = torch.zeros((70, cols + 48), dtype=torch.bfloat16, device=DEV)
+    xd[:, :cols] = x.to(DEV)
+    codes, scales = fp8q.quantize(xd[:, :cols], fp8q.ROW)
+    torch.cuda.synchronize()
+    oc, os_ = oracle.quantize(synth.bf16_bits(x), oracle.ROW)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint32), os_.view(np.uint32))
+    assert np.array_equal(codes.cpu().numpy(), oc)
+
+
 def test_padded_leading_dimensions():
     x = synth.activations(200, 512, seed=21, outlier_seed=22)
     xd = torch.zeros((200, 640), dtype=torch.bfloat16, device=DEV)
@@ -177,6 +192,9 @@ def test_full_8b_rowwise_operands():
     check(x.cpu(), fp8q.ROW, label="X rowwise")
     w = synth.weights(12288, 4096, seed=synth.seed_for(3, 1), device=DEV)
     check(w.cpu(), fp8q.ROW, label="W rowwise")
+    # the down projection's weight: rows of 12288
+    wd = synth.weights(4096, 12288, seed=synth.seed_for(3, 1, 1), device=DEV)
+    check(wd.cpu(), fp8q.ROW, label="W down rowwise")
 
 
 def test_full_32b_backward_operands():
