@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   // 128 x 128 tiles: thread (rg, cc) takes rows 8 rg .. 8 rg + 7.  Either
   // way a thread holds 8 rows x 8 columns, and the 16 lanes of a DPP row
   // share the thread's rows and cover 128 consecutive columns.
-  constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow);
+  constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow || K == kPreTensor);
   const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
   const int64_t tr = blockIdx.y, tc = blockIdx.x, tiles_r = gridDim.y, tiles_c = gridDim.x;
   const int64_t r0 = tr * (kWide ? kWideRows : kTile);
@@ -383,6 +383,31 @@ __global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) 
   }
 }
 
+// Amax pass of TENSOR: a grid-stride walk over 32 x 512 tiles (1 KB row
+// pieces per load instruction) keeping a running max per thread, then one
+// atomic max per workgroup (an atomic per tile would queue thousands of
+// them on the one address).
+__global__ __launch_bounds__(kThreads) void amax_tensor_kernel(QuantArgs a) {
+  __shared__ float lds4[4];
+  const int64_t tiles_c = (a.cols + kWideCols - 1) / kWideCols;
+  const int64_t tiles = tiles_c * ((a.rows + kWideRows - 1) / kWideRows);
+  float m = 0.0f;
+  for (int64_t t = blockIdx.x; t < tiles; t += gridDim.x) {
+    const int64_t r0 = (t / tiles_c) * kWideRows, c0 = (t % tiles_c) * kWideCols;
+    Tile p;
+    load_patch(a, r0 + (threadIdx.x >> 6) * 8, c0 + ((threadIdx.x >> 4) & 3) * 128 + (threadIdx.x & 15) * 8, p);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m = fmaxf(m, row_partial_max(p, i));
+  }
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    m = fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3]));
+    atomicMax(reinterpret_cast<unsigned int*>(a.scales), __float_as_uint(m));
+  }
+}
+
 __global__ void fill_zero_kernel(float* p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0.0f;
@@ -402,7 +427,7 @@ __global__ void cast_f32_kernel(const float* x, int64_t n, float scale, uint8_t*
 
 template <int K, bool TRANS>
 hipError_t launch_tile(const QuantArgs& a, hipStream_t s) {
-  constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow);
+  constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow || K == kPreTensor);
   constexpr int64_t tr = kWide ? kWideRows : kTile, tc = kWide ? kWideCols : kTile;
   const dim3 grid((unsigned)((a.cols + tc - 1) / tc), (unsigned)((a.rows + tr - 1) / tr));
   quant_tile_kernel<K, TRANS><<<grid, kThreads, 0, s>>>(a);
@@ -415,8 +440,13 @@ hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipS
   fill_zero_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const dim3 grid((unsigned)((a.cols + kTile - 1) / kTile), (unsigned)((a.rows + kTile - 1) / kTile));
-  amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a);
+  if (K == kPreTensor) {
+    const int64_t tiles = ((a.cols + kWideCols - 1) / kWideCols) * ((a.rows + kWideRows - 1) / kWideRows);
+    amax_tensor_kernel<<<(unsigned)(tiles < 2048 ? tiles : 2048), kThreads, 0, s>>>(a);
+  } else {
+    const dim3 grid((unsigned)((a.cols + kTile - 1) / kTile), (unsigned)((a.rows + kTile - 1) / kTile));
+    amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   e = trans ? launch_tile<K, true>(a, s) : launch_tile<K, false>(a, s);
   if (e != hipSuccess) return e;
