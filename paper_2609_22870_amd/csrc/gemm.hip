@@ -44,10 +44,13 @@ __device__ __forceinline__ v4f mfma_16x16x128(const v8i& a, const v8i& b, const 
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// Two floats to two bf16 (round to nearest even), packed low then high: one
+// v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((v2f{lo, hi}), v2bf));
 }
 
 // Buffer resource over `bytes` bytes at `base` (gfx9 raw buffer: stride 0,
@@ -643,10 +646,28 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   // tile holds BN bf16; its 16-byte chunk c sits at chunk c ^ (m & 15), which
   // keeps both the 8-byte writes (16 rows, same columns) and the 16-byte
   // reads (one row) free of bank conflicts.
+  // The rounding runs before the barrier, so that it overlaps the wait for
+  // the slowest wave and the last MFMAs.
   static_assert(BM * BN * 2 <= kStages * kStage, "C tile must fit in the LDS stages");
   const int voff_m = (lane & 15) * 4, voff_n = (lane >> 4) * 16;
   float st = 1.0f;
   if (PAIR == kPairTensor) st = load_f32(rsA, 0, 0) * load_f32(rsB, 0, 0);
+  uint2 packed[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i) {
+    const float sm = PAIR == kPairRow ? load_f32(rsA, voff_m + i * 64, mw * 4) : 1.0f;
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      float v[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[r] = acc[i][j][r];
+        if (PAIR == kPairTensor) v[r] = v[r] * st;
+        if (PAIR == kPairRow) v[r] = (v[r] * sm) * load_f32(rsB, voff_n + j * 64 + r * 4, nw * 4);
+      }
+      packed[i][j] = make_uint2(bf16x2_rne(v[0], v[1]), bf16x2_rne(v[2], v[3]));
+    }
+  }
   wait_vmem_all();  // no load may still be writing LDS
   __syncthreads();  // every wave is done with the operand stages
   constexpr int kRowBytes = BN * 2;
@@ -654,21 +675,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 #pragma unroll
   for (int i = 0; i < TI; ++i) {
     const int mt = wm + i * 16 + (lane & 15);  // row within the tile
-    const float sm = PAIR == kPairRow ? load_f32(rsA, voff_m + i * 64, mw * 4) : 1.0f;
 #pragma unroll
     for (int j = 0; j < TJ; ++j) {
       const int nt = wn + j * 16 + (lane >> 4) * 4;  // column within the tile
-      uint32_t h[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float v = acc[i][j][r];
-        if (PAIR == kPairTensor) v = v * st;
-        if (PAIR == kPairRow) v = (v * sm) * load_f32(rsB, voff_n + j * 64 + r * 4, nw * 4);
-        h[r] = bf16_rne(v);
-      }
       const int chunk = (nt * 2) >> 4, half = ((nt * 2) >> 3) & 1;
       *reinterpret_cast<uint2*>(lds + mt * kRowBytes + ((chunk ^ (mt & kChunkMask)) << 4) + half * 8) =
-          make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+          packed[i][j];
     }
   }
   __syncthreads();
