@@ -35,6 +35,8 @@ def parse():
                    help="untimed steps first (the clock settles over the first few dozen)")
     p.add_argument("--workload", default="8b_ffn_up_fwd_blockwise", choices=sorted(WORKLOADS))
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-extras", action="store_true",
+                   help="skip the timings of the kernels outside the step (backward-pass quantizer)")
     p.add_argument("--cpu-rows", type=int, default=4096,
                    help="rows of X the oracle processes for the CPU baseline")
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -132,6 +134,41 @@ def cpu_baseline(x, w, M, K, N, rows):
                   "128x128; %.1f s wall (%.1f s quantize, %.1f s GEMM)"
                   % (rows, M, wrows, N, t_step, t_quant, t_gemm),
     }
+
+
+def time_extras(torch, fp8q, synth, dev, reps=20):
+    """Kernels next to the step, each timed alone with HIP events on the
+    launch stream: the dual-layout quantizer of the backward pass on the
+    32B FFN output gradient dY[16384, 25600] (its 1x128 codes for dgrad and
+    its transposed 128x1 codes for wgrad from one read), against the two
+    single-layout calls it replaces."""
+    rows, cols = 16384, 25600
+    dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
+    outs = fp8q.quantize_dual(dy)
+    r1 = fp8q.quantize(dy, fp8q.BLOCK_1x128)
+    r2 = fp8q.quantize(dy, fp8q.BLOCK_128x1, transposed=True)
+    stream = torch.cuda.current_stream(dev)
+
+    def timed(f):
+        for _ in range(3):
+            f()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        for _ in range(reps):
+            f()
+        e.record(stream)
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / reps * 1000.0
+
+    t_dual = timed(lambda: fp8q.quantize_dual(dy, *outs))
+    t_two = timed(lambda: (fp8q.quantize(dy, fp8q.BLOCK_1x128, codes=r1[0], scales=r1[1]),
+                           fp8q.quantize(dy, fp8q.BLOCK_128x1, transposed=True, codes=r2[0], scales=r2[1])))
+    nbytes = 4.0 * rows * cols + 4.0 * (outs[1].numel() + outs[3].numel())
+    gbs = nbytes / (t_dual * 1e-6) / 1e9
+    return {"quantize_dual_32b_dy": {
+        "shape": [rows, cols], "us": round(t_dual, 1), "gbs": round(gbs, 1),
+        "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+        "algorithmic_bytes": round(nbytes), "two_single_layout_calls_us": round(t_two, 1)}}
 
 
 def main():
@@ -234,6 +271,8 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if not args.no_extras:
+        out["extra_kernels"] = time_extras(torch, fp8q, synth, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x.cpu(), w.cpu(), M, K, N, args.cpu_rows)
     print(json.dumps(out), flush=True)

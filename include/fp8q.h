@@ -104,6 +104,29 @@ fp8q_status fp8q_quantize(const void *x, int64_t rows, int64_t cols,
                           struct ihipStream_t *stream);
 
 /*
+ * Both operand layouts the backward pass needs, from one read of x (Eq. 3
+ * applied twice per element).  The weight-gradient GEMM contracts over the
+ * token dimension, so it takes x (an activation X or an output gradient dY)
+ * transposed and grouped by 128 along the rows, while the forward and
+ * data-gradient GEMMs take it grouped by 128 along the columns.  Outputs:
+ *   codes_r, scales_r  exactly fp8q_quantize(x, FP8Q_BLOCK_1x128, 0):
+ *                      codes [rows][ldc_r] (ldc_r >= cols), scales
+ *                      [cols/128][rows]
+ *   codes_t, scales_t  exactly fp8q_quantize(x, FP8Q_BLOCK_128x1,
+ *                      FP8Q_OUT_TRANSPOSED): codes [cols][ldc_t] (ldc_t >=
+ *                      rows), scales [rows/128][cols]
+ * x is bf16 [rows][ldx].  Shape rules: rows % 128 == 0 and cols % 128 == 0
+ * (else FP8Q_ERR_UNSUPPORTED).  Alignment: x and both code arrays 16-byte
+ * aligned, ldx % 8 == 0, ldc_r % 16 == 0, ldc_t % 16 == 0, scales 4-byte
+ * aligned (else FP8Q_ERR_ALIGN).  The four outputs must not overlap.
+ */
+fp8q_status fp8q_quantize_dual(const void *x, int64_t rows, int64_t cols,
+                               int64_t ldx, uint8_t *codes_r, int64_t ldc_r,
+                               float *scales_r, uint8_t *codes_t,
+                               int64_t ldc_t, float *scales_t,
+                               struct ihipStream_t *stream);
+
+/*
  * The FP8 linear layer's GEMM on dequantized operands (Eq. 3 applied to
  * both; fp32 accumulation; bf16 round-to-nearest-even output):
  *   C[m][n] = sum_k (S_A(m,k) A[m][k]) (S_B(n,k) B[n][k])

@@ -21,8 +21,8 @@ OUT_TRANSPOSED = 1
 _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
            -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
 # the entry points of include/fp8q.h
-EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_gemm", "fp8q_cast_f32",
-           "fp8q_status_string")
+EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
+           "fp8q_gemm", "fp8q_cast_f32", "fp8q_status_string")
 
 
 class Fp8qError(RuntimeError):
@@ -47,6 +47,8 @@ def lib():
         L.fp8q_scales_count.restype = i64
         L.fp8q_quantize.argtypes = [p, i64, i64, i64, i32, u32, p, i64, p, p]
         L.fp8q_quantize.restype = i32
+        L.fp8q_quantize_dual.argtypes = [p, i64, i64, i64, p, i64, p, p, i64, p, p]
+        L.fp8q_quantize_dual.restype = i32
         L.fp8q_gemm.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
                                 p, i64, p]
         L.fp8q_gemm.restype = i32
@@ -111,6 +113,31 @@ def quantize(x, granularity, transposed=False, codes=None, scales=None):
                              _stream(x))
     _check(st, "fp8q_quantize")
     return codes, scales
+
+
+def quantize_dual(x, codes_r=None, scales_r=None, codes_t=None, scales_t=None):
+    """Both backward-pass layouts of a bf16 CUDA tensor x[rows, cols] from
+    one read: (codes_r, scales_r) = quantize(x, BLOCK_1x128) and
+    (codes_t, scales_t) = quantize(x, BLOCK_128x1, transposed=True)."""
+    if x.dtype != torch.bfloat16 or not x.is_cuda:
+        raise ValueError("x must be a bf16 CUDA tensor")
+    rows, cols = x.shape
+    if codes_r is None:
+        codes_r = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
+    if scales_r is None:
+        scales_r = torch.empty(scales_count(rows, cols, BLOCK_1x128),
+                               dtype=torch.float32, device=x.device)
+    if codes_t is None:
+        codes_t = torch.empty((cols, rows), dtype=torch.uint8, device=x.device)
+    if scales_t is None:
+        scales_t = torch.empty(scales_count(rows, cols, BLOCK_128x1, True),
+                               dtype=torch.float32, device=x.device)
+    st = lib().fp8q_quantize_dual(x.data_ptr(), rows, cols, _ld(x),
+                                  codes_r.data_ptr(), _ld(codes_r),
+                                  scales_r.data_ptr(), codes_t.data_ptr(),
+                                  _ld(codes_t), scales_t.data_ptr(), _stream(x))
+    _check(st, "fp8q_quantize_dual")
+    return codes_r, scales_r, codes_t, scales_t
 
 
 def gemm(a, sa, ga, b, sb, gb, out=None):

@@ -74,6 +74,30 @@ fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx
   return from_hip(fp8q::launch_quantize(a, g, t, n, reinterpret_cast<hipStream_t>(stream)));
 }
 
+fp8q_status fp8q_quantize_dual(const void* x, int64_t rows, int64_t cols, int64_t ldx, uint8_t* codes_r,
+                               int64_t ldc_r, float* scales_r, uint8_t* codes_t, int64_t ldc_t, float* scales_t,
+                               struct ihipStream_t* stream) {
+  if (!x || !codes_r || !scales_r || !codes_t || !scales_t) return FP8Q_ERR_INVAL;
+  if (rows <= 0 || cols <= 0 || ldx < cols || ldc_r < cols || ldc_t < rows) return FP8Q_ERR_INVAL;
+  if (rows % 128 || cols % 128) return FP8Q_ERR_UNSUPPORTED;
+  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
+  if (!aligned(x, 16) || !aligned(codes_r, 16) || !aligned(codes_t, 16) || !aligned(scales_r, 4) ||
+      !aligned(scales_t, 4) || ldx % 8 || ldc_r % 16 || ldc_t % 16)
+    return FP8Q_ERR_ALIGN;
+  fp8q::DualArgs d;
+  d.a.x = static_cast<const uint16_t*>(x);
+  d.a.rows = rows;
+  d.a.cols = cols;
+  d.a.ldx = ldx;
+  d.a.codes = codes_r;
+  d.a.ldc = ldc_r;
+  d.a.scales = scales_r;
+  d.codes_t = codes_t;
+  d.ldc_t = ldc_t;
+  d.scales_t = scales_t;
+  return from_hip(fp8q::launch_quantize_dual(d, reinterpret_cast<hipStream_t>(stream)));
+}
+
 fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
                       const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
                       void* C, int64_t ldc, struct ihipStream_t* stream) {

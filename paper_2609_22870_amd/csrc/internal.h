@@ -19,6 +19,19 @@ hipError_t launch_quantize(const QuantArgs& a, int granularity, bool transposed,
                            hipStream_t s);
 hipError_t launch_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, hipStream_t s);
 
+// Both backward-pass layouts from one read: `a` carries x and the 1x128
+// output (codes [rows][ldc], scales [cols/128][rows]); codes_t / scales_t
+// take the 128x1 output written transposed (codes [cols][ldc_t], scales
+// [rows/128][cols]).
+struct DualArgs {
+  QuantArgs a;
+  uint8_t* codes_t;
+  int64_t ldc_t;
+  float* scales_t;
+};
+
+hipError_t launch_quantize_dual(const DualArgs& d, hipStream_t s);
+
 struct GemmArgs {
   const uint8_t* A;  // E4M3 [M][lda]
   const uint8_t* B;  // E4M3 [N][ldb]

@@ -138,6 +138,101 @@ __device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8]
     encode_all([](float x, float s_, float r_) { return slow_quotient(x, s_, r_); });
 }
 
+// Per-unit scales when a thread's eight rows are eight units shared by the
+// 16 lanes of its DPP row: lane cc of the row group holds the amax of row
+// cc % 8, computes that unit's S and 1/S (two IEEE divisions), and the
+// group exchanges them by lane shuffles.
+__device__ __forceinline__ void share_row_units(float amax, UnitScale& mine, float (&su)[8], float (&ru)[8]) {
+  const int lane = threadIdx.x & 63;
+  mine = unit_scale(amax);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    su[i] = __shfl(mine.s, (lane & 48) | i, 64);
+    ru[i] = __shfl(mine.r, (lane & 48) | i, 64);
+  }
+}
+
+// Per-unit scales when a thread's eight columns are eight units: thread
+// (rg < 8, cc) holds the amax of column 8 cc + rg, computes its S and 1/S,
+// and the block exchanges them through LDS (the upper half of lds_red, after
+// every read of its lower half).
+__device__ __forceinline__ void share_col_units(float amax, float* lds_red, UnitScale& mine, float (&su)[8],
+                                                float (&ru)[8]) {
+  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  mine = unit_scale(amax);
+  float2* lds_su = reinterpret_cast<float2*>(lds_red + 2 * kTile);
+  __syncthreads();
+  if (rg < 8) lds_su[cc * 8 + rg] = make_float2(mine.s, mine.r);
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float2 v = lds_su[cc * 8 + j];
+    su[j] = v.x;
+    ru[j] = v.y;
+  }
+}
+
+// The 1x128 amax of the row this lane computes (row cc % 8 of its eight):
+// each tile row is one 128-column unit spread over a 16-lane DPP row.
+__device__ __forceinline__ float block_row_amax(const Tile& t) {
+  const int cc = threadIdx.x & 15;
+  float am[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) am[i] = row16_max(row_partial_max(t, i));
+  float amax = am[0];
+#pragma unroll
+  for (int i = 1; i < 8; ++i) amax = (cc & 7) == i ? am[i] : amax;
+  return amax;
+}
+
+// Codes of the thread's 8 x 8 patch in the input's layout: rows row0 ..
+// row0+7, columns c .. c+7.
+__device__ __forceinline__ void store_patch(const uint32_t (&packed)[8][2], uint8_t* codes, int64_t ldc, int64_t rows,
+                                            int64_t cols, int64_t row0, int64_t c) {
+  if (c < cols) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t r = row0 + i;
+      if (r < rows) *reinterpret_cast<uint2*>(codes + r * ldc + c) = make_uint2(packed[i][0], packed[i][1]);
+    }
+  }
+}
+
+// Codes of a 128 x 128 tile at (r0, c0) written transposed, codes[c][r],
+// through LDS: LDS row = tile column (128 bytes = 16 chunks of 8 rows);
+// chunk rg of LDS row 8*cc+j is stored at chunk rg ^ cc, which spreads the
+// 16 lanes of a DPP row over all 32 banks.  Each output row then goes out as
+// 16-byte pieces.
+__device__ __forceinline__ void store_patch_transposed(const uint32_t (&packed)[8][2], uint64_t* lds_t,
+                                                       uint8_t* codes, int64_t ldc, int64_t rows, int64_t cols,
+                                                       int64_t r0, int64_t c0) {
+  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lo |= ((packed[i][j >> 2] >> (8 * (j & 3))) & 0xffu) << (8 * i);
+#pragma unroll
+    for (int i = 4; i < 8; ++i) hi |= ((packed[i][j >> 2] >> (8 * (j & 3))) & 0xffu) << (8 * (i - 4));
+    const int lrow = cc * 8 + j;
+    lds_t[lrow * 16 + (rg ^ cc)] = (uint64_t)lo | ((uint64_t)hi << 32);
+  }
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const int orow = p * 32 + (threadIdx.x >> 3);  // tile column = output row
+    const int qd = threadIdx.x & 7;                // 16-byte chunk of the output row
+    const int sw = orow >> 3;
+    const uint64_t a0 = lds_t[orow * 16 + ((2 * qd) ^ sw)];
+    const uint64_t a1 = lds_t[orow * 16 + ((2 * qd + 1) ^ sw)];
+    const int64_t oc = c0 + orow;
+    const int64_t orr = r0 + qd * 16;
+    if (oc < cols && orr < rows)
+      *reinterpret_cast<uint4*>(codes + oc * ldc + orr) =
+          make_uint4((uint32_t)a0, (uint32_t)(a0 >> 32), (uint32_t)a1, (uint32_t)(a1 >> 32));
+  }
+}
+
 template <int K, bool TRANS>
 __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   __shared__ float lds_red[4 * kTile];
@@ -170,28 +265,17 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   // block exchanges through LDS.
   constexpr bool by_row = K == kBlock1x128 || K == kPreRow;
   constexpr bool by_col = K == kBlock128x1 || K == kPreCol;
-  const int lane = threadIdx.x & 63;
   UnitScale mine;  // the unit this thread computes (eight-unit case)
   float su[8], ru[8];
   if (by_row) {
     float amax;
     if (K == kBlock1x128) {
-      float am[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) am[i] = row16_max(row_partial_max(t, i));
-      amax = am[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) amax = (cc & 7) == i ? am[i] : amax;
+      amax = block_row_amax(t);
     } else {
       const int64_t r = row0 + (cc & 7);
       amax = r < a.rows ? a.scales[r] : 0.0f;
     }
-    mine = unit_scale(amax);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      su[i] = __shfl(mine.s, (lane & 48) | i, 64);
-      ru[i] = __shfl(mine.r, (lane & 48) | i, 64);
-    }
+    share_row_units(amax, mine, su, ru);
   } else if (by_col) {
     float amax;
     if (K == kBlock128x1) {
@@ -204,18 +288,7 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       const int64_t cj = c0 + cc * 8 + (rg & 7);
       amax = cj < a.cols ? a.scales[cj] : 0.0f;
     }
-    mine = unit_scale(amax);
-    // exchange through LDS (after tile_col_max's reads of lds_red are done)
-    float2* lds_su = reinterpret_cast<float2*>(lds_red + 2 * kTile);
-    __syncthreads();
-    if (rg < 8) lds_su[cc * 8 + rg] = make_float2(mine.s, mine.r);
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float2 v = lds_su[cc * 8 + j];
-      su[j] = v.x;
-      ru[j] = v.y;
-    }
+    share_col_units(amax, lds_red, mine, su, ru);
   } else {
     mine = unit_scale(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0]);
 #pragma unroll
@@ -228,44 +301,10 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   uint32_t packed[8][2];
   encode_patch<by_row ? kUnitRow : (by_col ? kUnitCol : kUnitOne)>(t, su, ru, packed);
 
-  if (!TRANS) {
-    if (c < a.cols) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int64_t r = row0 + i;
-        if (r < a.rows)
-          *reinterpret_cast<uint2*>(a.codes + r * a.ldc + c) = make_uint2(packed[i][0], packed[i][1]);
-      }
-    }
-  } else {
-    // Transpose through LDS: LDS row = tile column (128 bytes = 16 chunks of
-    // 8 rows); chunk rg of LDS row 8*cc+j is stored at chunk rg ^ cc, which
-    // spreads the 16 lanes of a DPP row over all 32 banks.
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      uint32_t lo = 0, hi = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) lo |= ((packed[i][j >> 2] >> (8 * (j & 3))) & 0xffu) << (8 * i);
-#pragma unroll
-      for (int i = 4; i < 8; ++i) hi |= ((packed[i][j >> 2] >> (8 * (j & 3))) & 0xffu) << (8 * (i - 4));
-      const int lrow = cc * 8 + j;
-      lds_t[lrow * 16 + (rg ^ cc)] = (uint64_t)lo | ((uint64_t)hi << 32);
-    }
-    __syncthreads();
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int orow = p * 32 + (threadIdx.x >> 3);  // tile column = output row
-      const int qd = threadIdx.x & 7;                // 16-byte chunk of the output row
-      const int sw = orow >> 3;
-      const uint64_t a0 = lds_t[orow * 16 + ((2 * qd) ^ sw)];
-      const uint64_t a1 = lds_t[orow * 16 + ((2 * qd + 1) ^ sw)];
-      const int64_t oc = c0 + orow;
-      const int64_t orr = r0 + qd * 16;
-      if (oc < a.cols && orr < a.rows)
-        *reinterpret_cast<uint4*>(a.codes + oc * a.ldc + orr) =
-            make_uint4((uint32_t)a0, (uint32_t)(a0 >> 32), (uint32_t)a1, (uint32_t)(a1 >> 32));
-    }
-  }
+  if (!TRANS)
+    store_patch(packed, a.codes, a.ldc, a.rows, a.cols, row0, c);
+  else
+    store_patch_transposed(packed, lds_t, a.codes, a.ldc, a.rows, a.cols, r0, c0);
 
   // scales of the block granularities (TENSOR / ROW / COL are finalized later)
   if (K == kBlock1x128) {
@@ -284,6 +323,47 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       a.scales[idx] = mine.s;
     }
   }
+}
+
+// Both operand layouts of the backward pass from one read.  A 128 x 128
+// tile is quantized twice: per 1x128 unit (its rows), with codes stored as
+// read and scales at (c / 128) * rows + r, and per 128x1 unit (its
+// columns), with codes stored transposed, codes_t[c][r], and scales at
+// (r / 128) * cols + c.  Each half is the single-layout kernel's work, so
+// each result is byte-identical to it.
+__global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
+  __shared__ float lds_red[4 * kTile];
+  __shared__ uint64_t lds_t[kTile * kTile / 8];
+  const QuantArgs& a = d.a;
+  const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int64_t tr = blockIdx.y;
+  const int64_t r0 = tr * kTile, c0 = (int64_t)blockIdx.x * kTile;
+  const int64_t row0 = r0 + rg * 8, c = c0 + cc * 8;
+
+  Tile t;
+  load_patch(a, row0, c, t);
+  uint32_t packed[8][2];
+  UnitScale mine;
+  float su[8], ru[8];
+
+  share_row_units(block_row_amax(t), mine, su, ru);
+  encode_patch<kUnitRow>(t, su, ru, packed);
+  store_patch(packed, a.codes, a.ldc, a.rows, a.cols, row0, c);
+  {
+    const int64_t r = row0 + cc;
+    if (cc < 8 && r < a.rows && c < a.cols) a.scales[(c >> 7) * a.rows + r] = mine.s;
+  }
+
+  float m[8];
+  tile_col_max(t, lds_red, m);
+  float amax = m[0];
+#pragma unroll
+  for (int j = 1; j < 8; ++j) amax = (rg & 7) == j ? m[j] : amax;
+  share_col_units(amax, lds_red, mine, su, ru);
+  encode_patch<kUnitCol>(t, su, ru, packed);
+  store_patch_transposed(packed, lds_t, d.codes_t, d.ldc_t, a.rows, a.cols, r0, c0);
+  const int64_t cj = c0 + cc * 8 + rg;
+  if (rg < 8 && cj < a.cols) d.scales_t[tr * a.cols + cj] = mine.s;
 }
 
 // Amax pass of the two-pass granularities: atomic max of |x| into `scales`
@@ -473,6 +553,12 @@ hipError_t launch_quantize(const QuantArgs& a, int granularity, bool trans, int6
     case 2: return launch_two_pass<kPreCol>(a, trans, nscales, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_quantize_dual(const DualArgs& d, hipStream_t s) {
+  const dim3 grid((unsigned)((d.a.cols + kTile - 1) / kTile), (unsigned)((d.a.rows + kTile - 1) / kTile));
+  quant_dual_kernel<<<grid, kThreads, 0, s>>>(d);
+  return hipGetLastError();
 }
 
 hipError_t launch_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, hipStream_t s) {

@@ -130,3 +130,25 @@ def test_no_cpu_fallback_when_library_missing(monkeypatch, tmp_path):
     monkeypatch.setattr(fp8q, "_lib", None)
     with pytest.raises(ImportError):
         fp8q.lib()
+
+
+def dual(L, x=FAKE, rows=256, cols=256, ldx=256, cr=FAKE, ldr=256, sr=FAKE,
+         ct=FAKE, ldt=256, st=FAKE):
+    return L.fp8q_quantize_dual(x, rows, cols, ldx, cr, ldr, sr, ct, ldt, st, None)
+
+
+def test_quantize_dual_rejections(L):
+    assert dual(L, x=None) == -1
+    assert dual(L, cr=None) == -1
+    assert dual(L, st=None) == -1
+    assert dual(L, rows=0) == -1
+    assert dual(L, ldx=128) == -1
+    assert dual(L, ldr=128) == -1
+    assert dual(L, rows=384, ldt=256) == -1                  # ldt < rows
+    assert dual(L, rows=272, ldt=272) == -2                  # rows % 128
+    assert dual(L, cols=400, ldx=400, ldr=400) == -2         # cols % 128
+    assert dual(L, x=FAKE + 2) == -3
+    assert dual(L, ct=FAKE + 8) == -3
+    assert dual(L, sr=FAKE + 1) == -3
+    assert dual(L, ldx=260) == -3
+    assert dual(L, ldt=264) == -3
