@@ -136,12 +136,16 @@ def cpu_baseline(x, w, M, K, N, rows):
     }
 
 
-def time_extras(torch, fp8q, synth, dev, reps=20):
+def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
     """Kernels next to the step, each timed alone with HIP events on the
-    launch stream: the dual-layout quantizer of the backward pass on the
-    32B FFN output gradient dY[16384, 25600] (its 1x128 codes for dgrad and
-    its transposed 128x1 codes for wgrad from one read), against the two
-    single-layout calls it replaces."""
+    launch stream:
+    * the dual-layout quantizer of the backward pass on the 32B FFN output
+      gradient dY[16384, 25600] (its 1x128 codes for dgrad and its
+      transposed 128x1 codes for wgrad from one read), against the two
+      single-layout calls it replaces;
+    * the step's GEMM with its output quantized per 1x128 block in the
+      epilogue (the next layer's activation operand), against the GEMM
+      followed by the quantizer on its bf16 output."""
     rows, cols = 16384, 25600
     dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
     outs = fp8q.quantize_dual(dy)
@@ -165,10 +169,25 @@ def time_extras(torch, fp8q, synth, dev, reps=20):
                            fp8q.quantize(dy, fp8q.BLOCK_128x1, transposed=True, codes=r2[0], scales=r2[1])))
     nbytes = 4.0 * rows * cols + 4.0 * (outs[1].numel() + outs[3].numel())
     gbs = nbytes / (t_dual * 1e-6) / 1e9
+    del dy, outs, r1, r2
+
+    M, N, K = xq.shape[0], wq.shape[0], xq.shape[1]
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    yq = torch.empty((M, N), dtype=torch.uint8, device=dev)
+    ys = torch.empty(fp8q.scales_count(M, N, fp8q.BLOCK_1x128), dtype=torch.float32, device=dev)
+    t_fused = timed(lambda: fp8q.gemm_quantized(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128,
+                                                codes=yq, scales=ys))
+    t_sep = timed(lambda: (fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y),
+                           fp8q.quantize(y, fp8q.BLOCK_1x128, codes=yq, scales=ys)))
+    tflops = 2.0 * M * N * K / (t_fused * 1e-6) / 1e12
     return {"quantize_dual_32b_dy": {
         "shape": [rows, cols], "us": round(t_dual, 1), "gbs": round(gbs, 1),
         "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
-        "algorithmic_bytes": round(nbytes), "two_single_layout_calls_us": round(t_two, 1)}}
+        "algorithmic_bytes": round(nbytes), "two_single_layout_calls_us": round(t_two, 1)},
+        "gemm_quantized_output_8b_ffn_up": {
+        "shape": [M, K, N], "us": round(t_fused, 1), "tflops": round(tflops, 1),
+        "frac_mfma": round(tflops / PEAK_FP8_TFLOPS, 4),
+        "gemm_then_quantize_us": round(t_sep, 1)}}
 
 
 def main():
@@ -272,7 +291,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if not args.no_extras:
-        out["extra_kernels"] = time_extras(torch, fp8q, synth, dev)
+        out["extra_kernels"] = time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x.cpu(), w.cpu(), M, K, N, args.cpu_rows)
     print(json.dumps(out), flush=True)

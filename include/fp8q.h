@@ -151,6 +151,26 @@ fp8q_status fp8q_gemm(const uint8_t *A, const float *sA, fp8q_granularity gA,
                       struct ihipStream_t *stream);
 
 /*
+ * fp8q_gemm followed by the quantization of its output, in one kernel: the
+ * next layer's activation operand (Eq. 3 with 1x128 units along N) without
+ * the bf16 round trip through memory.  The outputs are exactly
+ *   fp8q_quantize(C, M, N, N, FP8Q_BLOCK_1x128, 0, codes, ldq, scales)
+ * for the bf16 C that fp8q_gemm computes from the same arguments:
+ *   codes   E4M3 [M][ldq], ldq >= N
+ *   scales  fp32 [N/128][M]
+ * Supported (gA, gB): (1x128, 128x128) only.  Shape rules: K % 128 == 0,
+ * N % 128 == 0.  Alignment: A, B and codes 16-byte aligned, lda, ldb and
+ * ldq multiples of 16, scales 4-byte aligned.
+ */
+fp8q_status fp8q_gemm_quantized(const uint8_t *A, const float *sA,
+                                fp8q_granularity gA, int64_t lda,
+                                const uint8_t *B, const float *sB,
+                                fp8q_granularity gB, int64_t ldb, int64_t M,
+                                int64_t N, int64_t K, uint8_t *codes,
+                                int64_t ldq, float *scales,
+                                struct ihipStream_t *stream);
+
+/*
  * Q_FP8(RN32(x[i] / scale)) for n fp32 values with one explicit scale: the
  * device rounding routine of fp8q_quantize exposed for exhaustive checks.
  * x and codes need no alignment beyond their element size; scale > 0.

@@ -22,7 +22,8 @@ _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
            -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
-           "fp8q_gemm", "fp8q_cast_f32", "fp8q_status_string")
+           "fp8q_gemm", "fp8q_gemm_quantized", "fp8q_cast_f32",
+           "fp8q_status_string")
 
 
 class Fp8qError(RuntimeError):
@@ -52,6 +53,9 @@ def lib():
         L.fp8q_gemm.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
                                 p, i64, p]
         L.fp8q_gemm.restype = i32
+        L.fp8q_gemm_quantized.argtypes = [p, p, i32, i64, p, p, i32, i64, i64,
+                                          i64, i64, p, i64, p, p]
+        L.fp8q_gemm_quantized.restype = i32
         L.fp8q_cast_f32.argtypes = [p, i64, ctypes.c_float, p, p]
         L.fp8q_cast_f32.restype = i32
         L.fp8q_status_string.argtypes = [i32]
@@ -157,6 +161,28 @@ def gemm(a, sa, ga, b, sb, gb, out=None):
                          out.data_ptr(), _ld(out), _stream(a))
     _check(st, "fp8q_gemm")
     return out
+
+
+def gemm_quantized(a, sa, ga, b, sb, gb, codes=None, scales=None):
+    """The GEMM of gemm() with its bf16 output quantized per 1x128 block
+    (the next layer's activation operand), in one kernel.  Returns (codes
+    uint8 [M, N], scales fp32 in the 1x128 layout), exactly
+    quantize(gemm(a, sa, ga, b, sb, gb), BLOCK_1x128)."""
+    M, K = a.shape
+    N, K2 = b.shape
+    if K != K2:
+        raise ValueError("contraction sizes differ")
+    if codes is None:
+        codes = torch.empty((M, N), dtype=torch.uint8, device=a.device)
+    if scales is None:
+        scales = torch.empty(scales_count(M, N, BLOCK_1x128), dtype=torch.float32,
+                             device=a.device)
+    st = lib().fp8q_gemm_quantized(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
+                                   b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
+                                   codes.data_ptr(), _ld(codes), scales.data_ptr(),
+                                   _stream(a))
+    _check(st, "fp8q_gemm_quantized")
+    return codes, scales
 
 
 def cast_f32(x, scale, codes=None):

@@ -137,7 +137,48 @@ fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, in
   g.sa_count = count_for(M, K, gA);
   g.sb_count = count_for(N, K, gB);
   g.c_aligned16 = aligned(C, 16) && ldc % 8 == 0;
+  g.Cq = nullptr;
+  g.Cs = nullptr;
+  g.ldq = 0;
+  g.cs_ld = 0;
   return from_hip(fp8q::launch_gemm(g, pair, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_gemm_quantized(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda,
+                                const uint8_t* B, const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M,
+                                int64_t N, int64_t K, uint8_t* codes, int64_t ldq, float* scales,
+                                struct ihipStream_t* stream) {
+  if (!A || !sA || !B || !sB || !codes || !scales) return FP8Q_ERR_INVAL;
+  if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
+  if (lda < K || ldb < K || ldq < N) return FP8Q_ERR_INVAL;
+  if (gA != FP8Q_BLOCK_1x128 || gB != FP8Q_BLOCK_128x128) return FP8Q_ERR_UNSUPPORTED;
+  if (K % 128 || N % 128) return FP8Q_ERR_UNSUPPORTED;
+  if (((M + 127) / 128) * (N / 128) > 0x7fffffff) return FP8Q_ERR_UNSUPPORTED;
+  if (!aligned(A, 16) || !aligned(B, 16) || lda % 16 || ldb % 16 || !aligned(codes, 16) || ldq % 16 ||
+      !aligned(sA, 4) || !aligned(sB, 4) || !aligned(scales, 4))
+    return FP8Q_ERR_ALIGN;
+  fp8q::GemmArgs g;
+  g.A = A;
+  g.B = B;
+  g.sA = sA;
+  g.sB = sB;
+  g.C = nullptr;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = N;
+  g.sa_ld = M;
+  g.sb_ld = N;
+  g.sa_count = count_for(M, K, gA);
+  g.sb_count = count_for(N, K, gB);
+  g.c_aligned16 = 0;
+  g.Cq = codes;
+  g.Cs = scales;
+  g.ldq = ldq;
+  g.cs_ld = M;
+  return from_hip(fp8q::launch_gemm_quantized(g, fp8q::kPairBlock, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, struct ihipStream_t* stream) {

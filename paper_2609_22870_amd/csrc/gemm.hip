@@ -248,9 +248,65 @@ __device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int b, int& tm
   tn = in_group / gsize;
 }
 
+// Quantized output: the tile's bf16 C, staged in LDS (row m at byte m *
+// ROW_BYTES, 16-byte chunk c at chunk c ^ (m & CHUNK_MASK)), quantized per
+// 1x128 unit along N by Eq. 3, exactly as the quantizer would quantize the
+// bf16 output: codes [M][ldq], scales [N/128][cs_ld] (the quantizer's 1x128
+// layout).  A thread takes chunk c (eight columns) of rows mt0 + p * RPP for
+// the PASSES passes p; the 16 chunks of one row's 128-column unit sit in the
+// 16 lanes of a DPP row, so a unit's amax is a DPP row max.  Lane j of the
+// DPP row then computes the S and 1/S of pass j's unit (two IEEE divisions
+// per lane, not per pass) and the lanes exchange them by shuffles.
+template <int PASSES, int ROW_BYTES, int CHUNK_MASK, int RPP>
+__device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t* lds, int64_t m0, int64_t n0,
+                                                int chunks_per_row) {
+  static_assert(PASSES <= 16, "one pass per lane of a DPP row");
+  const int lane = threadIdx.x & 63, j = lane & 15;
+  const int c = threadIdx.x % chunks_per_row, mt0 = threadIdx.x / chunks_per_row;
+  const int64_t n = n0 + c * 8;
+  uint4 v[PASSES];
+  float am[PASSES];
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const int mt = mt0 + p * RPP;
+    v[p] = *reinterpret_cast<const uint4*>(lds + mt * ROW_BYTES + ((c ^ (mt & CHUNK_MASK)) << 4));
+    const uint32_t w[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
+    float m = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) m = fmaxf(m, fmaxf(fabsf(bf16_lo(w[e])), fabsf(bf16_hi(w[e]))));
+    am[p] = row16_max(m);
+  }
+  float amax = am[0];
+#pragma unroll
+  for (int p = 1; p < PASSES; ++p) amax = j == p ? am[p] : amax;
+  const UnitScale mine = unit_scale(amax);
+  const bool fast = __all(j >= PASSES || mine.fast);
+#pragma unroll
+  for (int p = 0; p < PASSES; ++p) {
+    const float s = __shfl(mine.s, (lane & 48) | p, 64), r = __shfl(mine.r, (lane & 48) | p, 64);
+    const UnitScale u{s, r, s >= 0x1p-90f};
+    const uint32_t w[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
+    float q[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float lo = bf16_lo(w[e]), hi = bf16_hi(w[e]);
+      q[2 * e] = fast ? fast_quotient(lo, s, r) : quotient(lo, u);
+      q[2 * e + 1] = fast ? fast_quotient(hi, s, r) : quotient(hi, u);
+    }
+    const uint32_t c0 = e4m3_pack2<true>(q[2], q[3], e4m3_pack2<false>(q[0], q[1], 0u));
+    const uint32_t c1 = e4m3_pack2<true>(q[6], q[7], e4m3_pack2<false>(q[4], q[5], 0u));
+    const int64_t m = m0 + mt0 + p * RPP;
+    if (m < g.M && n < g.N) *reinterpret_cast<uint2*>(g.Cq + m * g.ldq + n) = make_uint2(c0, c1);
+  }
+  const int64_t m = m0 + mt0 + j * RPP;
+  if (j < PASSES && m < g.M && n < g.N) g.Cs[(n >> 7) * g.cs_ld + m] = mine.s;
+}
+
 // One workgroup computes a BM x BN tile of C with (BM/WM) x (BN/WN) waves,
-// each owning WM x WN as (WM/16) x (WN/16) MFMA tiles of 16 x 16.
-template <int PAIR, int BM, int BN, int WM, int WN>
+// each owning WM x WN as (WM/16) x (WN/16) MFMA tiles of 16 x 16.  QOUT: the
+// tile leaves as E4M3 codes and 1x128 scales of its bf16 values (see
+// store_quantized) instead of bf16.
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
   constexpr int kWavesN = BN / WN;
   constexpr int kWaves = (BM / WM) * kWavesN;
@@ -687,6 +743,11 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   constexpr int kChunksPerRow = kRowBytes / 16;
   constexpr int kThreads = kWaves * 64;
   constexpr int kRowsPerPass = kThreads / kChunksPerRow;
+  if constexpr (QOUT) {
+    static_assert(kChunksPerRow % 16 == 0, "a 128-column unit per DPP row");
+    store_quantized<BM / kRowsPerPass, kRowBytes, kChunkMask, kRowsPerPass>(g, lds, m0, n0, kChunksPerRow);
+    return;
+  }
   const int c = threadIdx.x % kChunksPerRow;
   const int64_t n = n0 + c * 8;
 #pragma unroll 4
@@ -714,41 +775,47 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   }
 }
 
-template <int PAIR, int BM, int BN, int WM, int WN>
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT>
 hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
   constexpr int threads = (BM / WM) * (BN / WN) * 64;
-  gemm_kernel<PAIR, BM, BN, WM, WN><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
+  gemm_kernel<PAIR, BM, BN, WM, WN, QOUT><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
   return hipGetLastError();
 }
 
 // 256 x 256 tiles (8 waves of 128 x 64) when they fill the chip at least
 // twice over; else 128 x 128 tiles (4 waves of 64 x 64) when they fill it
 // once; else 64 x 64 tiles (4 waves of 32 x 32), for skinny problems such as
-// a decode step, whose time goes into streaming the weights.
-template <int PAIR>
+// a decode step, whose time goes into streaming the weights.  Quantized
+// output needs whole 128-column units in a tile: 256 or 128 tiles only.
+template <int PAIR, bool QOUT>
 hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
   const int64_t mid_tiles = ((g.M + 127) / 128) * ((g.N + 127) / 128);
   if constexpr (PAIR != kPairBlockK) {
-    if (big_tiles >= 512) return launch_tiles<PAIR, 256, 256, 128, 64>(g, s);
+    if (big_tiles >= 512) return launch_tiles<PAIR, 256, 256, 128, 64, QOUT>(g, s);
   }
-  if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64>(g, s);
-  return launch_tiles<PAIR, 64, 64, 32, 32>(g, s);
+  if constexpr (QOUT) {
+    return launch_tiles<PAIR, 128, 128, 64, 64, QOUT>(g, s);
+  } else {
+    if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64, QOUT>(g, s);
+    return launch_tiles<PAIR, 64, 64, 32, 32, QOUT>(g, s);
+  }
 }
 
 // The kernels address operands with 32-bit offsets: split the problem into
 // sub-GEMMs whose A and B row ranges each span less than 4 GiB.
-template <int PAIR>
+template <int PAIR, bool QOUT>
 hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
   // 32-bit offsets: each sub-problem's A rows, B rows and C rows span
   // < 2 GiB, and row / column indices stay below 2^31 / 4
   const int64_t lim = (int64_t)1 << 31;
   int64_t mstep = g.M, nstep = g.N;
   if (g.M * g.lda >= lim) mstep = ((lim - 1) / g.lda) / 256 * 256;
-  if (g.M * g.ldc * 2 >= lim) {
-    const int64_t cstep = ((lim - 1) / (2 * g.ldc)) / 256 * 256;
+  const int64_t c_row_bytes = QOUT ? g.ldq : 2 * g.ldc;
+  if (g.M * c_row_bytes >= lim) {
+    const int64_t cstep = ((lim - 1) / c_row_bytes) / 256 * 256;
     if (cstep < mstep) mstep = cstep;
   }
   if (g.N * g.ldb >= lim) nstep = ((lim - 1) / g.ldb) / 256 * 256;
@@ -762,7 +829,12 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
       sub.N = (g.N - n) < nstep ? (g.N - n) : nstep;
       sub.A = g.A + m * g.lda;
       sub.B = g.B + n * g.ldb;
-      sub.C = g.C + m * g.ldc + n;
+      if (QOUT) {
+        sub.Cq = g.Cq + m * g.ldq + n;
+        sub.Cs = g.Cs + (n / 128) * g.cs_ld + m;  // n is a multiple of 256
+      } else {
+        sub.C = g.C + m * g.ldc + n;
+      }
       // scale arrays keep the full problem's layout (strides sa_ld, sb_ld);
       // re-base them at the sub-problem's first row / column
       int64_t da = 0, db = 0;
@@ -773,7 +845,7 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
       sub.sB = g.sB + db;
       sub.sa_count = g.sa_count - da;
       sub.sb_count = g.sb_count - db;
-      hipError_t e = launch_pair<PAIR>(sub, s);
+      hipError_t e = launch_pair<PAIR, QOUT>(sub, s);
       if (e != hipSuccess) return e;
     }
   }
@@ -783,7 +855,7 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
 // Explicit instantiations: the host pass otherwise emits launch stubs only
 // for the first instantiated pair.
 #define FP8Q_GEMM_KERNEL(PAIR, BM, BN, WM, WN) \
-  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN>(GemmArgs);
+  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN, false>(GemmArgs);
 FP8Q_GEMM_KERNEL(kPairTensor, 256, 256, 128, 64)
 FP8Q_GEMM_KERNEL(kPairTensor, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairRow, 256, 256, 128, 64)
@@ -796,6 +868,8 @@ FP8Q_GEMM_KERNEL(kPairRow, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairBlock, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairBlockK, 64, 64, 32, 32)
 #undef FP8Q_GEMM_KERNEL
+template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true>(GemmArgs);
+template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true>(GemmArgs);
 
 }  // namespace gemm_detail
 
@@ -803,12 +877,17 @@ using namespace gemm_detail;
 
 hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s) {
   switch (pair) {
-    case kPairTensor: return launch_split<kPairTensor>(g, s);
-    case kPairRow: return launch_split<kPairRow>(g, s);
-    case kPairBlock: return launch_split<kPairBlock>(g, s);
-    case kPairBlockK: return launch_split<kPairBlockK>(g, s);
+    case kPairTensor: return launch_split<kPairTensor, false>(g, s);
+    case kPairRow: return launch_split<kPairRow, false>(g, s);
+    case kPairBlock: return launch_split<kPairBlock, false>(g, s);
+    case kPairBlockK: return launch_split<kPairBlockK, false>(g, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s) {
+  if (pair != kPairBlock || g.N % 128) return hipErrorInvalidValue;
+  return launch_split<kPairBlock, true>(g, s);
 }
 
 }  // namespace fp8q

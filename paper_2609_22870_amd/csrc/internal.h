@@ -46,10 +46,16 @@ struct GemmArgs {
   int64_t sa_count, sb_count;
   // C and ldc allow 16-byte stores (else 8-byte)
   int c_aligned16;
+  // quantized output (fp8q_gemm_quantized): E4M3 codes [M][ldq] and 1x128
+  // scales [N/128][cs_ld] of the bf16 result (cs_ld: the whole problem's M)
+  uint8_t* Cq;
+  float* Cs;
+  int64_t ldq, cs_ld;
 };
 
 enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3 };
 
 hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s);
+hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s);
 
 }  // namespace fp8q

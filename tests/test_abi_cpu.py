@@ -152,3 +152,23 @@ def test_quantize_dual_rejections(L):
     assert dual(L, sr=FAKE + 1) == -3
     assert dual(L, ldx=260) == -3
     assert dual(L, ldt=264) == -3
+
+
+def gemm_q(L, A=FAKE, sA=FAKE, gA=3, lda=256, B=FAKE, sB=FAKE, gB=5, ldb=256,
+           M=256, N=256, K=256, q=FAKE, ldq=256, s=FAKE):
+    return L.fp8q_gemm_quantized(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, q, ldq, s, None)
+
+
+def test_gemm_quantized_rejections(L):
+    assert gemm_q(L, A=None) == -1
+    assert gemm_q(L, q=None) == -1
+    assert gemm_q(L, s=None) == -1
+    assert gemm_q(L, M=0) == -1
+    assert gemm_q(L, ldq=128) == -1
+    assert gemm_q(L, gA=0, gB=0) == -2                       # only 1x128 x 128x128
+    assert gemm_q(L, gA=3, gB=3) == -2
+    assert gemm_q(L, K=200, lda=256, ldb=256) == -2
+    assert gemm_q(L, N=200, ldq=256) == -2
+    assert gemm_q(L, q=FAKE + 8) == -3
+    assert gemm_q(L, ldq=264) == -3
+    assert gemm_q(L, s=FAKE + 2) == -3
