@@ -19,6 +19,10 @@ shapes of those models:
 
 M = 16384 tokens is one 16K-context sequence; M = 256 is one decode step over
 256 sequences.
+
+For Calibrated Clipping (Sec. 4, Alg. 1) the inputs are per-token arrays of
+one GRPO training batch (Appendix setup: 256 prompts, 8 responses each, 16K
+context); see rl_batch.
 """
 import torch
 
@@ -90,3 +94,37 @@ def grads(M, N, seed, device="cpu"):
 def bf16_bits(t):
     """bf16 tensor -> numpy uint16 bit patterns (CPU copy)."""
     return t.detach().cpu().contiguous().view(torch.int16).numpy().view("uint16")
+
+
+# GRPO batch of the paper's 8B setup: prompts x responses per prompt, with
+# response lengths drawn uniformly from [RL_MIN_LEN, RL_MAX_LEN] tokens.
+RL_BATCH = dict(prompts=256, group=8)
+RL_MIN_LEN, RL_MAX_LEN = 512, 8192
+
+
+def rl_batch(prompts, group, seed, min_len=RL_MIN_LEN, max_len=RL_MAX_LEN, zero_adv=0.1,
+             ratio_sigma=0.05, fp8_sigma=0.03, tis_sigma=0.02, tis_cap=2.0, device="cpu"):
+    """Per-token float32 inputs of Calibrated Clipping for one batch, as a
+    dict of 1-D tensors (adv, w_tis, pi_sampler, r_bf16, r_fp8), responses
+    laid out one after another.  Stand-ins drawn from a seeded generator:
+
+    * each response has one advantage for all its tokens, N(0, 1), or 0 for
+      a fraction `zero_adv` of the responses (groups whose rewards all agree);
+    * sampler token probabilities 1 / (1 + exp(-z)), z ~ N(3, 2);
+    * BF16 importance ratios exp(N(0, ratio_sigma)); FP8 ratios are the BF16
+      ones times exp(N(0, fp8_sigma)), the quantization noise;
+    * TIS weights min(exp(N(0, tis_sigma)), tis_cap).
+    """
+    g = torch.Generator().manual_seed(seed)
+    n_resp = prompts * group
+    lens = torch.randint(min_len, max_len + 1, (n_resp,), generator=g)
+    adv_resp = torch.randn(n_resp, generator=g)
+    adv_resp[torch.rand(n_resp, generator=g) < zero_adv] = 0.0
+    adv = torch.repeat_interleave(adv_resp, lens)
+    n = adv.numel()
+    pi = torch.sigmoid(3.0 + 2.0 * torch.randn(n, generator=g))
+    r_bf16 = torch.exp(ratio_sigma * torch.randn(n, generator=g))
+    r_fp8 = r_bf16 * torch.exp(fp8_sigma * torch.randn(n, generator=g))
+    w = torch.clamp(torch.exp(tis_sigma * torch.randn(n, generator=g)), max=tis_cap)
+    out = dict(adv=adv, w_tis=w, pi_sampler=pi, r_bf16=r_bf16, r_fp8=r_fp8)
+    return {k: v.to(torch.float32).contiguous().to(device) for k, v in out.items()}
