@@ -145,7 +145,10 @@ def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
       single-layout calls it replaces;
     * the step's GEMM with its output quantized per 1x128 block in the
       epilogue (the next layer's activation operand), against the GEMM
-      followed by the quantizer on its bf16 output."""
+      followed by the quantizer on its bf16 output;
+    * Calibrated Clipping (Alg. 1) over one batch of the paper's GRPO setup
+      (256 prompts x 8 responses of 512-8192 tokens: 8.9 M tokens, five
+      float32 arrays), both of its kernels."""
     rows, cols = 16384, 25600
     dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
     outs = fp8q.quantize_dual(dy)
@@ -180,6 +183,17 @@ def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
     t_sep = timed(lambda: (fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y),
                            fp8q.quantize(y, fp8q.BLOCK_1x128, codes=yq, scales=ys)))
     tflops = 2.0 * M * N * K / (t_fused * 1e-6) / 1e12
+    del y, yq, ys
+
+    rl = {k: v.to(dev) for k, v in synth.rl_batch(**synth.RL_BATCH, seed=5001).items()}
+    keys = ("adv", "w_tis", "pi_sampler", "r_bf16", "r_fp8")
+    ntok = rl["adv"].numel()
+    ws = torch.empty(fp8q.lib().fp8q_calibrate_clip_workspace(ntok), dtype=torch.uint8, device=dev)
+    res = torch.empty(80, dtype=torch.uint8, device=dev)
+    t_clip = timed(lambda: fp8q.calibrate_clip(*(rl[k] for k in keys), 0.6, 1.8, workspace=ws,
+                                               result=res, read=False))
+    clip_bytes = 20.0 * ntok
+    clip_gbs = clip_bytes / (t_clip * 1e-6) / 1e9
     return {"quantize_dual_32b_dy": {
         "shape": [rows, cols], "us": round(t_dual, 1), "gbs": round(gbs, 1),
         "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
@@ -187,7 +201,10 @@ def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
         "gemm_quantized_output_8b_ffn_up": {
         "shape": [M, K, N], "us": round(t_fused, 1), "tflops": round(tflops, 1),
         "frac_mfma": round(tflops / PEAK_FP8_TFLOPS, 4),
-        "gemm_then_quantize_us": round(t_sep, 1)}}
+        "gemm_then_quantize_us": round(t_sep, 1)},
+        "calibrated_clipping_grpo_batch": {
+        "tokens": ntok, "us": round(t_clip, 1), "gbs": round(clip_gbs, 1),
+        "frac_hbm": round(clip_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": round(clip_bytes)}}
 
 
 def main():

@@ -171,6 +171,70 @@ fp8q_status fp8q_gemm_quantized(const uint8_t *A, const float *sA,
                                 struct ihipStream_t *stream);
 
 /*
+ * Calibrated Clipping (Sec. 4, Alg. 1, Eq. 5): new lower and upper PPO
+ * clipping bounds for FP8 training from one batch of n tokens.
+ *
+ * Inputs, float32 device arrays of n tokens, 16-byte aligned: adv (the
+ * advantage A_t), w_tis (the TIS weight, already truncated), pi_sampler
+ * (the sampler's probability of the token), r_bf16 and r_fp8 (the
+ * importance ratio from the BF16 shadow passes and from the FP8 passes).
+ * Ratios must be finite.  l_old, h_old: the current bounds.  config (a HOST
+ * pointer, read during the call): the reference bounds, the search
+ * intervals and step, and the SmoothUpdate limits; PAPER values in the
+ * field comments.
+ *
+ * Steps (each statistic is a float64 sum over the batch):
+ *   alpha_low = F_BF16,-(c_low_ref), F the CDF P(r <= x) over tokens with
+ *               A < 0;
+ *   L* = grid point of [l_min, l_max] minimising |F_FP8,-(L) - alpha_low|;
+ *   rho(c_low, c_high) = |sum_{A>0} w pi r A [r < c_high]| /
+ *                        |sum_{A<0} w pi r A [r > c_low]|   (Eq. 5);
+ *   H* = grid point of [h_min, h_max] minimising |rho_FP8(L*, H) -
+ *        rho_BF16(c_low_ref, c_high_ref)|;
+ *   new bound = b + clip((b* - b) / 2, -delta, delta)   (SmoothUpdate).
+ * Grid points are lo + k * step (float64, no fused multiply-add), k = 0 ..
+ * round((hi - lo) / step); ties go to the first point.  Tokens with A = 0
+ * count nowhere.  With no negative-advantage token both bounds stay; when
+ * an Eq. 5 denominator is zero the upper bound stays.  Results are the same
+ * on every run.
+ *
+ * workspace: device memory of at least fp8q_calibrate_clip_workspace(n)
+ * bytes, 8-byte aligned, overwritten.  result: a DEVICE pointer to one
+ * fp8q_clip_result (8-byte aligned), written by the last kernel; fields of
+ * a stage that did not run are NaN.  Errors: null pointers, n <= 0, step
+ * <= 0, empty or inverted intervals, a span that is not a whole number of
+ * steps, or a small workspace -> INVAL; grids of more than 24 (lower) or
+ * 48 (upper) points -> UNSUPPORTED; misaligned arrays -> ALIGN.
+ */
+typedef struct fp8q_clip_config {
+  double c_low_ref, c_high_ref; /* reference bounds (paper, GRPO: 0.8, 1.24) */
+  double l_min, l_max;          /* search interval of L (paper: 0.5, 0.9)     */
+  double h_min, h_max;          /* search interval of H (paper: 1.2, 2.0)     */
+  double step;                  /* search step (paper: 0.02)                  */
+  double delta_l, delta_h;      /* SmoothUpdate limits (paper: 0.05, 0.1)     */
+} fp8q_clip_config;
+
+typedef struct fp8q_clip_result {
+  double l_new, h_new;     /* the updated bounds                          */
+  double l_star, h_star;   /* the grid optima                             */
+  double alpha_low;        /* F_BF16,-(c_low_ref)                         */
+  double rho_bf16;         /* Eq. 5 of the BF16 ratios at the references */
+  double rho_fp8;          /* Eq. 5 of the FP8 ratios at (L*, H*)         */
+  int64_t n_neg, n_pos;    /* tokens with A < 0, A > 0                    */
+  int32_t l_updated, h_updated;
+} fp8q_clip_result;
+
+int64_t fp8q_calibrate_clip_workspace(int64_t n);
+
+fp8q_status fp8q_calibrate_clip(const float *adv, const float *w_tis,
+                                const float *pi_sampler, const float *r_bf16,
+                                const float *r_fp8, int64_t n, double l_old,
+                                double h_old, const fp8q_clip_config *config,
+                                void *workspace, int64_t workspace_bytes,
+                                fp8q_clip_result *result,
+                                struct ihipStream_t *stream);
+
+/*
  * Q_FP8(RN32(x[i] / scale)) for n fp32 values with one explicit scale: the
  * device rounding routine of fp8q_quantize exposed for exhaustive checks.
  * x and codes need no alignment beyond their element size; scale > 0.

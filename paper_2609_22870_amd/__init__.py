@@ -22,8 +22,27 @@ _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
            -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
-           "fp8q_gemm", "fp8q_gemm_quantized", "fp8q_cast_f32",
-           "fp8q_status_string")
+           "fp8q_gemm", "fp8q_gemm_quantized", "fp8q_calibrate_clip_workspace",
+           "fp8q_calibrate_clip", "fp8q_cast_f32", "fp8q_status_string")
+
+
+class ClipConfig(ctypes.Structure):
+    """fp8q_clip_config (include/fp8q.h)."""
+    _fields_ = [(n, ctypes.c_double) for n in ("c_low_ref", "c_high_ref", "l_min", "l_max",
+                                                "h_min", "h_max", "step", "delta_l", "delta_h")]
+
+
+class ClipResult(ctypes.Structure):
+    """fp8q_clip_result (include/fp8q.h)."""
+    _fields_ = ([(n, ctypes.c_double) for n in ("l_new", "h_new", "l_star", "h_star", "alpha_low",
+                                                 "rho_bf16", "rho_fp8")]
+                + [("n_neg", ctypes.c_int64), ("n_pos", ctypes.c_int64),
+                   ("l_updated", ctypes.c_int32), ("h_updated", ctypes.c_int32)])
+
+
+# Sec. 4 settings, with the GRPO experiments' reference bounds (Sec. 5.1).
+PAPER_CLIP_CONFIG = dict(c_low_ref=0.8, c_high_ref=1.24, l_min=0.5, l_max=0.9, h_min=1.2,
+                         h_max=2.0, step=0.02, delta_l=0.05, delta_h=0.1)
 
 
 class Fp8qError(RuntimeError):
@@ -56,6 +75,12 @@ def lib():
         L.fp8q_gemm_quantized.argtypes = [p, p, i32, i64, p, p, i32, i64, i64,
                                           i64, i64, p, i64, p, p]
         L.fp8q_gemm_quantized.restype = i32
+        L.fp8q_calibrate_clip_workspace.argtypes = [i64]
+        L.fp8q_calibrate_clip_workspace.restype = i64
+        d = ctypes.c_double
+        L.fp8q_calibrate_clip.argtypes = [p, p, p, p, p, i64, d, d, ctypes.POINTER(ClipConfig),
+                                          p, i64, p, p]
+        L.fp8q_calibrate_clip.restype = i32
         L.fp8q_cast_f32.argtypes = [p, i64, ctypes.c_float, p, p]
         L.fp8q_cast_f32.restype = i32
         L.fp8q_status_string.argtypes = [i32]
@@ -183,6 +208,37 @@ def gemm_quantized(a, sa, ga, b, sb, gb, codes=None, scales=None):
                                    _stream(a))
     _check(st, "fp8q_gemm_quantized")
     return codes, scales
+
+
+def calibrate_clip(adv, w_tis, pi_sampler, r_bf16, r_fp8, l_old, h_old, config=None,
+                   workspace=None, result=None, read=True):
+    """Calibrated Clipping (Alg. 1) on the GPU.  The five per-token inputs
+    are contiguous float32 CUDA tensors of one batch; config maps the
+    fields of ClipConfig (default: the paper's).  Returns the result as a
+    dict (reading it back waits for the kernels); `result` may be a uint8
+    CUDA tensor of ctypes.sizeof(ClipResult) bytes to write into, and with
+    read=False nothing is read back (the call returns None)."""
+    ts = (adv, w_tis, pi_sampler, r_bf16, r_fp8)
+    n = adv.numel()
+    for t in ts:
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous() or t.numel() != n:
+            raise ValueError("inputs must be contiguous float32 CUDA tensors of one length")
+    cfg = ClipConfig(**(config or PAPER_CLIP_CONFIG))
+    need = lib().fp8q_calibrate_clip_workspace(n)
+    if need < 0:
+        raise ValueError("empty batch")
+    if workspace is None:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=adv.device)
+    if result is None:
+        result = torch.empty(ctypes.sizeof(ClipResult), dtype=torch.uint8, device=adv.device)
+    st = lib().fp8q_calibrate_clip(*(t.data_ptr() for t in ts), n, float(l_old), float(h_old),
+                                   ctypes.byref(cfg), workspace.data_ptr(), workspace.numel(),
+                                   result.data_ptr(), _stream(adv))
+    _check(st, "fp8q_calibrate_clip")
+    if not read:
+        return None
+    r = ClipResult.from_buffer_copy(result.cpu().numpy().tobytes())
+    return {name: getattr(r, name) for name, _ in ClipResult._fields_}
 
 
 def cast_f32(x, scale, codes=None):

@@ -36,6 +36,26 @@ int64_t count_for(int64_t rows, int64_t cols, int g) {
 
 fp8q_status from_hip(hipError_t e) { return e == hipSuccess ? FP8Q_OK : FP8Q_ERR_HIP; }
 
+// Calibrated Clipping: one block per `chunk` consecutive tokens, at most
+// kClipMaxBlocks (one per CU), chunks a multiple of 1024 tokens (up to 256
+// threads x 4).
+void clip_blocks(int64_t n, int64_t& chunk, int64_t& blocks) {
+  int64_t c = (n + fp8q::kClipMaxBlocks - 1) / fp8q::kClipMaxBlocks;
+  c = (c + 1023) / 1024 * 1024;
+  chunk = c < 4096 ? 4096 : c;
+  blocks = (n + chunk - 1) / chunk;
+}
+
+// Points lo + k step, k = 0 .. round((hi - lo) / step), when the span is a
+// whole number of steps (to 1e-9 of a step).
+bool grid_size(double lo, double hi, double step, int& n) {
+  const double q = (hi - lo) / step;
+  const double k = nearbyint(q);
+  if (!(fabs(q - k) <= 1e-9) || k > 1e6) return false;
+  n = (int)k + 1;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -179,6 +199,55 @@ fp8q_status fp8q_gemm_quantized(const uint8_t* A, const float* sA, fp8q_granular
   g.ldq = ldq;
   g.cs_ld = M;
   return from_hip(fp8q::launch_gemm_quantized(g, fp8q::kPairBlock, reinterpret_cast<hipStream_t>(stream)));
+}
+
+int64_t fp8q_calibrate_clip_workspace(int64_t n) {
+  if (n <= 0) return -1;
+  int64_t chunk, blocks;
+  clip_blocks(n, chunk, blocks);
+  return blocks * fp8q::clip_slots(fp8q::kClipMaxL, fp8q::kClipMaxH) * (int64_t)sizeof(double);
+}
+
+fp8q_status fp8q_calibrate_clip(const float* adv, const float* w_tis, const float* pi_sampler, const float* r_bf16,
+                                const float* r_fp8, int64_t n, double l_old, double h_old,
+                                const fp8q_clip_config* config, void* workspace, int64_t workspace_bytes,
+                                fp8q_clip_result* result, struct ihipStream_t* stream) {
+  if (!adv || !w_tis || !pi_sampler || !r_bf16 || !r_fp8 || !config || !workspace || !result) return FP8Q_ERR_INVAL;
+  if (n <= 0) return FP8Q_ERR_INVAL;
+  const fp8q_clip_config c = *config;
+  if (!(c.step > 0.0) || !(c.l_max >= c.l_min) || !(c.h_max >= c.h_min)) return FP8Q_ERR_INVAL;
+  int nl, nh;
+  if (!grid_size(c.l_min, c.l_max, c.step, nl) || !grid_size(c.h_min, c.h_max, c.step, nh)) return FP8Q_ERR_INVAL;
+  if (nl > fp8q::kClipMaxL || nh > fp8q::kClipMaxH) return FP8Q_ERR_UNSUPPORTED;
+  if (workspace_bytes < fp8q_calibrate_clip_workspace(n)) return FP8Q_ERR_INVAL;
+  if (!aligned(adv, 16) || !aligned(w_tis, 16) || !aligned(pi_sampler, 16) || !aligned(r_bf16, 16) ||
+      !aligned(r_fp8, 16) || !aligned(workspace, 8) || !aligned(result, 8))
+    return FP8Q_ERR_ALIGN;
+  fp8q::ClipArgs p;
+  p.adv = adv;
+  p.w = w_tis;
+  p.pi = pi_sampler;
+  p.rb = r_bf16;
+  p.rf = r_fp8;
+  p.n = n;
+  int64_t blocks;
+  clip_blocks(n, p.chunk, blocks);
+  p.blocks = (int)blocks;
+  p.nl = nl;
+  p.nh = nh;
+  p.c_low_ref = c.c_low_ref;
+  p.c_high_ref = c.c_high_ref;
+  p.l_min = c.l_min;
+  p.h_min = c.h_min;
+  p.step = c.step;
+  p.inv_step = 1.0 / c.step;
+  p.delta_l = c.delta_l;
+  p.delta_h = c.delta_h;
+  p.l_old = l_old;
+  p.h_old = h_old;
+  p.partials = static_cast<double*>(workspace);
+  p.result = result;
+  return from_hip(fp8q::launch_calibrate_clip(p, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, struct ihipStream_t* stream) {

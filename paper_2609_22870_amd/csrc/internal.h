@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fp8q.h"
+
 namespace fp8q {
 
 struct QuantArgs {
@@ -57,5 +59,27 @@ enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3 }
 
 hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s);
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s);
+
+// Calibrated Clipping: per-token float32 arrays of n tokens, the grids
+// l_min + k step (k < nl) and h_min + k step (k < nh), and a workspace of
+// blocks x clip_slots(nl, nh) float64 partial sums (one block per `chunk`
+// consecutive tokens).  The result goes to device memory.
+constexpr int kClipMaxL = 24, kClipMaxH = 48;
+constexpr int kClipMaxBlocks = 256;
+
+struct ClipArgs {
+  const float *adv, *w, *pi, *rb, *rf;
+  int64_t n, chunk;
+  int blocks, nl, nh;
+  double c_low_ref, c_high_ref, l_min, h_min, step, inv_step, delta_l, delta_h, l_old, h_old;
+  double* partials;
+  fp8q_clip_result* result;
+};
+
+using ClipResult = fp8q_clip_result;
+
+// float64 slots per block for these grid sizes (-1 when unsupported)
+int clip_slots(int nl, int nh);
+hipError_t launch_calibrate_clip(const ClipArgs& p, hipStream_t s);
 
 }  // namespace fp8q

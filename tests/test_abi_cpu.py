@@ -172,3 +172,29 @@ def test_gemm_quantized_rejections(L):
     assert gemm_q(L, q=FAKE + 8) == -3
     assert gemm_q(L, ldq=264) == -3
     assert gemm_q(L, s=FAKE + 2) == -3
+
+
+def calib(L, ptrs=(FAKE,) * 5, n=4096, cfg=None, ws=FAKE, ws_bytes=1 << 30, res=FAKE):
+    import ctypes
+    c = fp8q.ClipConfig(**(cfg or fp8q.PAPER_CLIP_CONFIG))
+    return L.fp8q_calibrate_clip(*ptrs, n, 0.6, 1.8, ctypes.byref(c), ws, ws_bytes, res, None)
+
+
+def test_calibrate_clip_workspace_and_rejections(L):
+    assert L.fp8q_calibrate_clip_workspace(0) == -1
+    assert L.fp8q_calibrate_clip_workspace(1) > 0
+    assert L.fp8q_calibrate_clip_workspace(1 << 30) >= L.fp8q_calibrate_clip_workspace(1 << 20)
+    P = fp8q.PAPER_CLIP_CONFIG
+    assert calib(L, ptrs=(None,) + (FAKE,) * 4) == -1
+    assert calib(L, ws=None) == -1
+    assert calib(L, res=None) == -1
+    assert calib(L, n=0) == -1
+    assert calib(L, cfg=dict(P, step=0.0)) == -1
+    assert calib(L, cfg=dict(P, l_max=0.4)) == -1                 # inverted interval
+    assert calib(L, cfg=dict(P, l_max=0.91)) == -1                # not whole steps
+    assert calib(L, ws_bytes=8) == -1
+    assert calib(L, cfg=dict(P, l_min=0.42)) == -2                # 25 lower points
+    assert calib(L, cfg=dict(P, h_max=2.16)) == -2                # 49 upper points
+    assert calib(L, ptrs=(FAKE + 4,) + (FAKE,) * 4) == -3
+    assert calib(L, ws=FAKE + 4) == -3
+    assert calib(L, res=FAKE + 4) == -3

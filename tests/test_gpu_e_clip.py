@@ -1,0 +1,107 @@
+"""GPU parity of Calibrated Clipping (paper Sec. 4, Alg. 1, Eq. 5) against
+the float64 oracle, through the C-ABI.
+
+Both sides take the same decisions: the lower-bound search compares integer
+counts (exact on both sides), and the upper-bound search compares float64
+ratios whose sums differ only in summation order (the GPU sums in a fixed
+tree), so the grid optima, the counts and the new bounds must be equal and
+the Eq. 5 ratios equal to 1e-12 relative."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_22870_amd as fp8q
+from paper_2609_22870_amd import synth
+from oracle import clip
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+KEYS = ("adv", "w_tis", "pi_sampler", "r_bf16", "r_fp8")
+
+
+def compare(b, l_old, h_old, config=None, label=""):
+    n = b["adv"].numel()
+    print("calibrated clipping parity", label, n, "tokens", flush=True)
+    cfg = config or clip.PAPER_CONFIG
+    got = fp8q.calibrate_clip(*(b[k].to(DEV) for k in KEYS), l_old, h_old, config=cfg)
+    want = clip.calibrate(*(b[k].numpy() for k in KEYS), l_old, h_old, cfg)
+    print("  L* %r H* %r -> [%r, %r]" % (got["l_star"], got["h_star"], got["l_new"], got["h_new"]), flush=True)
+    assert got["n_neg"] == want["n_neg"] and got["n_pos"] == want["n_pos"]
+    assert bool(got["l_updated"]) == want["l_updated"] and bool(got["h_updated"]) == want["h_updated"]
+    for k in ("l_star", "h_star", "alpha_low"):
+        if want[k] is None:
+            assert math.isnan(got[k]), k
+        else:
+            assert got[k] == want[k], (k, got[k], want[k])
+    for k in ("rho_bf16", "rho_fp8"):
+        if want[k] is None:
+            assert math.isnan(got[k]), k
+        else:
+            assert abs(got[k] - want[k]) <= 1e-12 * abs(want[k]), (k, got[k], want[k])
+    assert got["l_new"] == want["l_new"] and got["h_new"] == want["h_new"]
+    return got
+
+
+def test_paper_batch():
+    """One batch of the paper's GRPO setup (256 prompts x 8 responses,
+    8.9 M tokens), bounds from the paper's initialisation."""
+    b = synth.rl_batch(**synth.RL_BATCH, seed=5001)
+    compare(b, 0.6, 1.8, label="paper batch")
+
+
+@pytest.mark.parametrize("seed,fp8_sigma,l_old,h_old", [(11, 0.03, 0.66, 1.5), (12, 0.1, 0.72, 1.3),
+                                                        (13, 0.2, 0.55, 1.95)])
+def test_smaller_batches(seed, fp8_sigma, l_old, h_old):
+    b = synth.rl_batch(32, 8, seed=seed, fp8_sigma=fp8_sigma)
+    compare(b, l_old, h_old, label="seed %d sigma %g" % (seed, fp8_sigma))
+
+
+@pytest.mark.parametrize("n", [1, 3, 1021, 4096 + 5, 3 * 5120 + 1])
+def test_ragged_lengths(n):
+    """Token counts that leave a partial 4-token group, a partial block, or
+    a single token."""
+    b = synth.rl_batch(4, 8, seed=21 + n, min_len=1, max_len=4000)
+    b = {k: v[:n].clone() for k, v in b.items()}
+    if b["adv"].numel() < n:
+        pytest.skip("batch shorter than %d" % n)
+    compare(b, 0.6, 1.8, label="n=%d" % n)
+
+
+def test_identical_ratios():
+    b = synth.rl_batch(16, 8, seed=31)
+    b["r_fp8"] = b["r_bf16"].clone()
+    got = compare(b, 0.6, 1.8, label="identical ratios")
+    assert got["l_star"] == 0.8 and got["h_star"] == 1.24
+
+
+def test_degenerate_batches():
+    b = synth.rl_batch(8, 8, seed=41)
+    b["adv"] = b["adv"].abs()                      # no negative advantage
+    got = compare(b, 0.62, 1.74, label="no negatives")
+    assert not got["l_updated"] and got["l_new"] == 0.62 and got["h_new"] == 1.74
+    b = synth.rl_batch(8, 8, seed=42)
+    b["adv"] = -b["adv"].abs() - 1e-3             # no positive advantage: rho = 0
+    compare(b, 0.62, 1.74, label="no positives")
+
+
+def test_general_grid():
+    """A grid beyond the paper's sizes (24 lower, 48 upper points) runs the
+    general instantiation; one more point is refused."""
+    cfg = dict(clip.PAPER_CONFIG, l_min=0.44, l_max=0.9, h_min=1.1, h_max=2.04)
+    b = synth.rl_batch(32, 8, seed=51, fp8_sigma=0.1)
+    compare(b, 0.6, 1.8, config=cfg, label="24 x 48 grid")
+    with pytest.raises(fp8q.Fp8qError):
+        fp8q.calibrate_clip(*(b[k].to(DEV) for k in KEYS), 0.6, 1.8,
+                            config=dict(cfg, l_min=0.42))
+
+
+def test_deterministic():
+    b = {k: v.to(DEV) for k, v in synth.rl_batch(64, 8, seed=61).items()}
+    res = [torch.empty(80, dtype=torch.uint8, device=DEV) for _ in range(2)]
+    for r in res:
+        fp8q.calibrate_clip(*(b[k] for k in KEYS), 0.6, 1.8, result=r)
+    torch.cuda.synchronize()
+    assert torch.equal(res[0], res[1])
