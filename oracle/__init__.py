@@ -21,6 +21,7 @@ SOURCES = ["e4m3.c", "quantize.c", "gemm.c"]
 
 TENSOR, ROW, COL, BLOCK_1x128, BLOCK_128x1, BLOCK_128x128 = range(6)
 OUT_TRANSPOSED = 1
+POW2_SCALE = 2
 
 
 def build(force=True):
@@ -89,8 +90,8 @@ def scale_count(rows, cols, granularity):
             BLOCK_128x128: (rows // 128) * (cols // 128)}[granularity]
 
 
-def quantize(x_bits, granularity, transposed=False):
-    """Eq. 3 per scaling unit.
+def quantize(x_bits, granularity, transposed=False, pow2=False):
+    """Eq. 3 per scaling unit (pow2: the power-of-two scale variant).
 
     x_bits: uint16 array [rows, cols] of bf16 bit patterns.
     Returns (codes uint8 [rows, cols] or [cols, rows], scales float32 1-D).
@@ -105,7 +106,7 @@ def quantize(x_bits, granularity, transposed=False):
     codes = np.empty((orows, ocols), dtype=np.uint8)
     scales = np.empty(scale_count(orows, ocols, og), dtype=np.float32)
     rc = lib().oracle_quantize(_ptr(x_bits), rows, cols, cols, granularity,
-                               OUT_TRANSPOSED if transposed else 0,
+                               (OUT_TRANSPOSED if transposed else 0) | (POW2_SCALE if pow2 else 0),
                                _ptr(codes), ocols, _ptr(scales))
     if rc != 0:
         raise ValueError("oracle_quantize rejected the arguments")

@@ -53,7 +53,7 @@ enum {
   ORACLE_BLOCK_128x1 = 4,
   ORACLE_BLOCK_128x128 = 5
 };
-enum { ORACLE_OUT_TRANSPOSED = 1 };
+enum { ORACLE_OUT_TRANSPOSED = 1, ORACLE_POW2_SCALE = 2 };
 
 /* Value of an OCP E4M3 byte; NaN for 0x7F and 0xFF. */
 double oracle_e4m3_decode(uint8_t code);

@@ -67,6 +67,18 @@ static float scale_from_amax(float amax) {
   return s;
 }
 
+/* The power-of-two variant (not the paper's scale): the smallest power of
+ * two S with 448 S >= amax, at least 2^-127, and 1 for amax = 0.  Found by
+ * exact comparisons of 448 * 2^k with amax in double. */
+static float pow2_scale_from_amax(float amax) {
+  if (amax == 0.0f) return 1.0f;
+  int k = ilogb(amax) - 8;
+  while (ldexp(448.0, k) < (double)amax) ++k;
+  while (ldexp(448.0, k - 1) >= (double)amax) --k;
+  if (k < -127) k = -127;
+  return (float)ldexp(1.0, k);
+}
+
 uint8_t oracle_cast_f32(float x, float scale) {
   float q = x / scale; /* one correctly rounded fp32 division */
   return oracle_e4m3_encode(q);
@@ -110,7 +122,9 @@ int oracle_quantize(const uint16_t *x_bf16, int64_t rows, int64_t cols,
     }
   }
   /* S of every unit */
-  for (int64_t u = 0; u < nunits; ++u) scales[u] = scale_from_amax(amax[u]);
+  int pow2 = (flags & ORACLE_POW2_SCALE) != 0;
+  for (int64_t u = 0; u < nunits; ++u)
+    scales[u] = pow2 ? pow2_scale_from_amax(amax[u]) : scale_from_amax(amax[u]);
   /* codes */
   for (int64_t r = 0; r < rows; ++r) {
     for (int64_t c = 0; c < cols; ++c) {

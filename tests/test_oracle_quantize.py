@@ -297,3 +297,66 @@ def test_division_not_reciprocal():
         assert scales[0] == S
         assert np.array_equal(codes[0, 1:1 + sel.size], c_div[diff[:127]])
     assert found > 50
+
+
+# ---- the power-of-two scale variant (not the paper's scale): S is the
+# smallest power of two with 448 S >= amax, at least 2^-127
+
+def exact_pow2_scale(amax):
+    """Smallest power of two S (as a Fraction exponent search) with 448 S >=
+    amax, clamped at 2^-127; 1 for amax = 0."""
+    from fractions import Fraction
+    a = Fraction(amax)
+    if a == 0:
+        return 1.0
+    k = 0
+    while 448 * Fraction(2) ** k < a:
+        k += 1
+    while 448 * Fraction(2) ** (k - 1) >= a:
+        k -= 1
+    return float(Fraction(2) ** max(k, -127))
+
+
+def test_pow2_scales_against_exact_search():
+    """Single-unit (tensorwise) quantizations of amaxes across the bf16
+    range, including 448 * 2^k and its bf16 neighbours, subnormals and the
+    largest finite bf16."""
+    amaxes = [448.0 * 2.0 ** k for k in range(-20, 20)]
+    amaxes += [float(torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).float() * f)
+               for v in (1.0, 3.0, 0.875, 0.9, 1.75, 1.7578125) for f in (1.0, 2.0 ** -60, 2.0 ** 70)]
+    amaxes += [2.0 ** -133, 2.0 ** -130, 1.5 * 2.0 ** -127, 3.3895313892515355e38, 0.0]
+    for amax in amaxes:
+        x = torch.tensor([[amax, -amax / 4.0]], dtype=torch.float32).to(torch.bfloat16)
+        a = float(x.float().abs().max())
+        _, s = oracle.quantize(bits(x), oracle.TENSOR, pow2=True)
+        assert float(s[0]) == exact_pow2_scale(a), (a, s[0])
+
+
+@pytest.mark.parametrize("g", G_ALL)
+def test_pow2_codes_are_exact_quotients(g):
+    """S is a power of two, so x / S is exact: every code is the nearest
+    E4M3 value of the exact quotient, no quotient exceeds 448, and the
+    dequantization error is at most half a unit in the last place."""
+    x = sample(256, 256, 23)
+    codes, scales = oracle.quantize(bits(x), g, pow2=True)
+    assert np.all(np.frexp(scales.astype(np.float64))[0] == 0.5)       # powers of two
+    table = np.array([oracle.decode(c) if c not in (0x7F, 0xFF) else np.nan for c in range(256)])
+    dec = table[codes]
+    # the unit geometry of the fp32 mode, with the power-of-two scales
+    s_plain, full_plain = expand_scales(x, g)
+    full = np.zeros_like(full_plain)
+    for v_plain, v_pow2 in zip(np.asarray(s_plain, dtype=np.float64), scales.astype(np.float64)):
+        full[full_plain == v_plain] = v_pow2
+    xf = x.float().numpy().astype(np.float64)
+    q = xf / full
+    assert np.all(np.abs(q) <= 448)
+    assert np.all(np.abs(xf - full * dec) <= full * np.maximum(2.0 ** -4 * np.abs(dec), 2.0 ** -10))
+
+
+def test_pow2_matches_plain_scale_when_amax_is_448_times_a_power_of_two():
+    """amax = 448 * 2^j makes both scales 2^j: identical codes and scales."""
+    x = sample(128, 256, 29, outliers=False)
+    x = plant_max(x, oracle.BLOCK_1x128, 448.0 * 2.0 ** -9)
+    c1, s1 = oracle.quantize(bits(x), oracle.BLOCK_1x128)
+    c2, s2 = oracle.quantize(bits(x), oracle.BLOCK_1x128, pow2=True)
+    assert np.array_equal(s1, s2) and np.array_equal(c1, c2)
