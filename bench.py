@@ -136,7 +136,7 @@ def cpu_baseline(x, w, M, K, N, rows):
     }
 
 
-def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
+def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
     """Kernels next to the step, each timed alone with HIP events on the
     launch stream:
     * the dual-layout quantizer of the backward pass on the 32B FFN output
@@ -148,7 +148,10 @@ def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
       followed by the quantizer on its bf16 output;
     * Calibrated Clipping (Alg. 1) over one batch of the paper's GRPO setup
       (256 prompts x 8 responses of 512-8192 tokens: 8.9 M tokens, five
-      float32 arrays), both of its kernels."""
+      float32 arrays), both of its kernels;
+    * the step's GEMM on operands quantized with power-of-two scales (a
+      variant, not the paper's scale), whose block scales enter the matrix
+      instruction, with that quantization of X."""
     rows, cols = 16384, 25600
     dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
     outs = fp8q.quantize_dual(dy)
@@ -183,7 +186,15 @@ def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
     t_sep = timed(lambda: (fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y),
                            fp8q.quantize(y, fp8q.BLOCK_1x128, codes=yq, scales=ys)))
     tflops = 2.0 * M * N * K / (t_fused * 1e-6) / 1e12
-    del y, yq, ys
+    del yq, ys
+
+    xb = torch.empty_like(xq)
+    sxb = torch.empty_like(sx)
+    wb, swb = fp8q.quantize(w, fp8q.BLOCK_128x128, pow2=True)
+    t_qx2 = timed(lambda: fp8q.quantize(x, fp8q.BLOCK_1x128, codes=xb, scales=sxb, pow2=True))
+    t_pow2 = timed(lambda: fp8q.gemm_pow2(xb, sxb, fp8q.BLOCK_1x128, wb, swb, fp8q.BLOCK_128x128, out=y))
+    pow2_tflops = 2.0 * M * N * K / (t_pow2 * 1e-6) / 1e12
+    del y, xb, sxb, wb, swb
 
     rl = {k: v.to(dev) for k, v in synth.rl_batch(**synth.RL_BATCH, seed=5001).items()}
     keys = ("adv", "w_tis", "pi_sampler", "r_bf16", "r_fp8")
@@ -202,6 +213,9 @@ def time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw, reps=20):
         "shape": [M, K, N], "us": round(t_fused, 1), "tflops": round(tflops, 1),
         "frac_mfma": round(tflops / PEAK_FP8_TFLOPS, 4),
         "gemm_then_quantize_us": round(t_sep, 1)},
+        "gemm_pow2_scales_8b_ffn_up": {
+        "shape": [M, K, N], "us": round(t_pow2, 1), "tflops": round(pow2_tflops, 1),
+        "frac_mfma": round(pow2_tflops / PEAK_FP8_TFLOPS, 4), "quantize_x_pow2_us": round(t_qx2, 1)},
         "calibrated_clipping_grpo_batch": {
         "tokens": ntok, "us": round(t_clip, 1), "gbs": round(clip_gbs, 1),
         "frac_hbm": round(clip_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": round(clip_bytes)}}
@@ -308,7 +322,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if not args.no_extras:
-        out["extra_kernels"] = time_extras(torch, fp8q, synth, dev, xq, sx, wq, sw)
+        out["extra_kernels"] = time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(x.cpu(), w.cpu(), M, K, N, args.cpu_rows)
     print(json.dumps(out), flush=True)

@@ -63,6 +63,11 @@ typedef enum {
  * units stay the same sets of elements; the scales are laid out for the
  * transposed matrix (so 1x128 of x is 128x1 of x^T, ROW of x is COL). */
 enum { FP8Q_OUT_TRANSPOSED = 1u };
+/* A variant of Eq. 3's scale (not the paper's; for fp8q_gemm_pow2): S is
+ * the smallest power of two with 448 S >= amax, at least 2^-127, and 1 when
+ * amax is 0.  Every |x| / S is then at most 448 and exact, and S fits the
+ * E8M0 block scales of the MI355X matrix instructions. */
+enum { FP8Q_POW2_SCALE = 2u };
 
 /*
  * Number of fp32 scales fp8q_quantize writes for an input of rows x cols
@@ -86,7 +91,8 @@ int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g,
                           unsigned flags);
 
 /*
- * Eq. 3 per scaling unit: codes and scales of x.
+ * Eq. 3 per scaling unit: codes and scales of x.  flags: FP8Q_OUT_TRANSPOSED,
+ * FP8Q_POW2_SCALE, or both.
  *   x       bf16 [rows][ldx], ldx >= cols
  *   codes   E4M3 [rows][ldc] (ldc >= cols), or [cols][ldc] (ldc >= rows)
  *           with FP8Q_OUT_TRANSPOSED
@@ -149,6 +155,21 @@ fp8q_status fp8q_gemm(const uint8_t *A, const float *sA, fp8q_granularity gA,
                       fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N,
                       int64_t K, void *C, int64_t ldc,
                       struct ihipStream_t *stream);
+
+/*
+ * fp8q_gemm for operands quantized with FP8Q_POW2_SCALE: the same product
+ * (fp32 accumulation, bf16 round-to-nearest-even output), with the block
+ * scales applied inside the matrix instruction as E8M0 exponents instead
+ * of by fp32 multiplies.  Every scale must be a power of two in [2^-127,
+ * 2^127] (as FP8Q_POW2_SCALE writes them; other values are read as their
+ * exponent alone).  Supported (gA, gB): (1x128, 128x128) only.  Shape and
+ * alignment rules: those of fp8q_gemm, with N % 128 == 0.
+ */
+fp8q_status fp8q_gemm_pow2(const uint8_t *A, const float *sA,
+                           fp8q_granularity gA, int64_t lda, const uint8_t *B,
+                           const float *sB, fp8q_granularity gB, int64_t ldb,
+                           int64_t M, int64_t N, int64_t K, void *C,
+                           int64_t ldc, struct ihipStream_t *stream);
 
 /*
  * fp8q_gemm followed by the quantization of its output, in one kernel: the

@@ -18,11 +18,12 @@ LIB_PATH = os.path.join(_HERE, "libfp8q.so")
 # fp8q_granularity
 TENSOR, ROW, COL, BLOCK_1x128, BLOCK_128x1, BLOCK_128x128 = range(6)
 OUT_TRANSPOSED = 1
+POW2_SCALE = 2
 _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
            -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
-           "fp8q_gemm", "fp8q_gemm_quantized", "fp8q_calibrate_clip_workspace",
+           "fp8q_gemm", "fp8q_gemm_pow2", "fp8q_gemm_quantized", "fp8q_calibrate_clip_workspace",
            "fp8q_calibrate_clip", "fp8q_cast_f32", "fp8q_status_string")
 
 
@@ -72,6 +73,8 @@ def lib():
         L.fp8q_gemm.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
                                 p, i64, p]
         L.fp8q_gemm.restype = i32
+        L.fp8q_gemm_pow2.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64, p, i64, p]
+        L.fp8q_gemm_pow2.restype = i32
         L.fp8q_gemm_quantized.argtypes = [p, p, i32, i64, p, p, i32, i64, i64,
                                           i64, i64, p, i64, p, p]
         L.fp8q_gemm_quantized.restype = i32
@@ -120,12 +123,12 @@ def scales_count(rows, cols, granularity, transposed=False):
     return n
 
 
-def quantize(x, granularity, transposed=False, codes=None, scales=None):
+def quantize(x, granularity, transposed=False, codes=None, scales=None, pow2=False):
     """Eq. 3 per scaling unit on a bf16 CUDA tensor x[rows, cols].
 
     Returns (codes, scales): codes uint8 (OCP E4M3 bytes) [rows, cols], or
     [cols, rows] when `transposed`; scales fp32 1-D in the layout of
-    include/fp8q.h.
+    include/fp8q.h.  pow2: power-of-two scales (FP8Q_POW2_SCALE).
     """
     if x.dtype != torch.bfloat16 or not x.is_cuda:
         raise ValueError("x must be a bf16 CUDA tensor")
@@ -137,7 +140,7 @@ def quantize(x, granularity, transposed=False, codes=None, scales=None):
         scales = torch.empty(scales_count(rows, cols, granularity, transposed),
                              dtype=torch.float32, device=x.device)
     st = lib().fp8q_quantize(x.data_ptr(), rows, cols, _ld(x), granularity,
-                             OUT_TRANSPOSED if transposed else 0,
+                             (OUT_TRANSPOSED if transposed else 0) | (POW2_SCALE if pow2 else 0),
                              codes.data_ptr(), _ld(codes), scales.data_ptr(),
                              _stream(x))
     _check(st, "fp8q_quantize")
@@ -185,6 +188,22 @@ def gemm(a, sa, ga, b, sb, gb, out=None):
                          b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                          out.data_ptr(), _ld(out), _stream(a))
     _check(st, "fp8q_gemm")
+    return out
+
+
+def gemm_pow2(a, sa, ga, b, sb, gb, out=None):
+    """gemm() for operands quantized with power-of-two scales (pow2=True):
+    the block scales enter the matrix instruction as exponents."""
+    M, K = a.shape
+    N, K2 = b.shape
+    if K != K2:
+        raise ValueError("contraction sizes differ")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    st = lib().fp8q_gemm_pow2(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
+                              b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
+                              out.data_ptr(), _ld(out), _stream(a))
+    _check(st, "fp8q_gemm_pow2")
     return out
 
 

@@ -61,7 +61,8 @@ bool grid_size(double lo, double hi, double step, int& n) {
 extern "C" {
 
 int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g, unsigned flags) {
-  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~FP8Q_OUT_TRANSPOSED)) return -1;
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~(FP8Q_OUT_TRANSPOSED | FP8Q_POW2_SCALE)))
+    return -1;
   const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
   const int64_t orows = t ? cols : rows, ocols = t ? rows : cols;
   return count_for(orows, ocols, t ? transposed_granularity(g) : g);
@@ -71,7 +72,7 @@ fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx
                           unsigned flags, uint8_t* codes, int64_t ldc, float* scales,
                           struct ihipStream_t* stream) {
   if (!x || !codes || !scales) return FP8Q_ERR_INVAL;
-  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~FP8Q_OUT_TRANSPOSED))
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~(FP8Q_OUT_TRANSPOSED | FP8Q_POW2_SCALE)))
     return FP8Q_ERR_INVAL;
   const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
   if (ldx < cols || ldc < (t ? rows : cols)) return FP8Q_ERR_INVAL;
@@ -90,6 +91,7 @@ fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx
   a.codes = codes;
   a.ldc = ldc;
   a.scales = scales;
+  a.pow2 = (flags & FP8Q_POW2_SCALE) != 0;
   const int64_t n = fp8q_scales_count(rows, cols, g, flags);
   return from_hip(fp8q::launch_quantize(a, g, t, n, reinterpret_cast<hipStream_t>(stream)));
 }
@@ -112,6 +114,7 @@ fp8q_status fp8q_quantize_dual(const void* x, int64_t rows, int64_t cols, int64_
   d.a.codes = codes_r;
   d.a.ldc = ldc_r;
   d.a.scales = scales_r;
+  d.a.pow2 = 0;
   d.codes_t = codes_t;
   d.ldc_t = ldc_t;
   d.scales_t = scales_t;
@@ -162,6 +165,42 @@ fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, in
   g.ldq = 0;
   g.cs_ld = 0;
   return from_hip(fp8q::launch_gemm(g, pair, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_gemm_pow2(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                           const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                           void* C, int64_t ldc, struct ihipStream_t* stream) {
+  if (!A || !sA || !B || !sB || !C) return FP8Q_ERR_INVAL;
+  if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
+  if (lda < K || ldb < K || ldc < N) return FP8Q_ERR_INVAL;
+  if (gA != FP8Q_BLOCK_1x128 || gB != FP8Q_BLOCK_128x128) return FP8Q_ERR_UNSUPPORTED;
+  if (K % 128 || N % 128) return FP8Q_ERR_UNSUPPORTED;
+  if (((M + 127) / 128) * (N / 128) > 0x7fffffff) return FP8Q_ERR_UNSUPPORTED;
+  if (!aligned(A, 16) || !aligned(B, 16) || lda % 16 || ldb % 16 || !aligned(C, 8) || ldc % 4 ||
+      !aligned(sA, 4) || !aligned(sB, 4))
+    return FP8Q_ERR_ALIGN;
+  fp8q::GemmArgs g;
+  g.A = A;
+  g.B = B;
+  g.sA = sA;
+  g.sB = sB;
+  g.C = static_cast<uint16_t*>(C);
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.lda = lda;
+  g.ldb = ldb;
+  g.ldc = ldc;
+  g.sa_ld = M;
+  g.sb_ld = N;
+  g.sa_count = count_for(M, K, gA);
+  g.sb_count = count_for(N, K, gB);
+  g.c_aligned16 = aligned(C, 16) && ldc % 8 == 0;
+  g.Cq = nullptr;
+  g.Cs = nullptr;
+  g.ldq = 0;
+  g.cs_ld = 0;
+  return from_hip(fp8q::launch_gemm(g, fp8q::kPairBlockE8, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_gemm_quantized(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda,

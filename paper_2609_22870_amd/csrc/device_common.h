@@ -30,6 +30,31 @@ __device__ __forceinline__ UnitScale unit_scale(float amax) {
   return u;
 }
 
+// The power-of-two variant: S = the smallest power of two with 448 S >=
+// amax, at least 2^-127 (the E8M0 range of the matrix instructions' block
+// scales), and 1 when amax is 0.  Then |x| / S <= 448 and x / S is exact.
+// With amax = m 2^e (m in [0.5, 1)), amax / 448 = (8 m / 7) 2^(e - 9), and
+// 8 m / 7 <= 1 exactly when m <= 7/8.
+__device__ __forceinline__ UnitScale unit_scale_pow2(float amax) {
+  UnitScale u;
+  if (amax == 0.0f) {
+    u.s = 1.0f;
+  } else {
+    int e;
+    const float m = frexpf(amax, &e);
+    int k = e - 9 + (m > 0.875f ? 1 : 0);
+    k = k < -127 ? -127 : k;
+    u.s = ldexpf(1.0f, k);
+  }
+  u.r = 1.0f / u.s;  // exact: a power of two
+  u.fast = u.s >= 0x1p-90f;
+  return u;
+}
+
+__device__ __forceinline__ UnitScale unit_scale(float amax, bool pow2) {
+  return pow2 ? unit_scale_pow2(amax) : unit_scale(amax);
+}
+
 // RN32(x / S) for a bf16 x of the unit whose scale is u.  For S >= 2^-90 the
 // quotient is formed from the reciprocal with one residual correction,
 //   q0 = RN(x r),  e = RN(q0 S - x) (one FMA),  q = RN(q0 - e r) (one FMA);

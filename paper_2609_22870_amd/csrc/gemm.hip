@@ -44,6 +44,19 @@ __device__ __forceinline__ v4f mfma_16x16x128(const v8i& a, const v8i& b, const 
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
+// The same with power-of-two block scales applied inside the instruction:
+// scale_a (of this lane) multiplies row l % 16 of `a` over its 32-deep K
+// piece l / 16, scale_b the same of `b`; each is an E8M0 byte (2^(e - 127),
+// e = 127 for 1.0; measured on gfx950 with runtime operands).
+__device__ __forceinline__ v4f mfma_16x16x128_e8(const v8i& a, const v8i& b, const v4f& c, int scale_a,
+                                                 int scale_b) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, scale_a, 0, scale_b);
+}
+
+// E8M0 byte of a power-of-two fp32 scale in [2^-127, 2^127]: its exponent
+// field (2^-127, an fp32 subnormal, has field 0, which E8M0 reads as 2^-127).
+__device__ __forceinline__ int e8m0_of(float pow2) { return (int)((__float_as_uint(pow2) >> 23) & 0xffu); }
+
 typedef float v2f __attribute__((ext_vector_type(2)));
 typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
 
@@ -312,12 +325,18 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   constexpr int kWaves = (BM / WM) * kWavesN;
   constexpr int TI = WM / 16, TJ = WN / 16;
   constexpr int kTileA = BM * kBK, kTileB = BN * kBK, kStage = kTileA + kTileB;
-  constexpr bool kBlockScaled = PAIR == kPairBlock || PAIR == kPairBlockK;
+  // kBlockScaled: per-K-step scale vectors are staged with the tiles;
+  // kPromote: they are applied by FMAs on the VALU (fp32 scales), else the
+  // accumulation runs in the MFMA accumulator (power-of-two scales enter
+  // the instruction itself)
+  constexpr bool kBlockScaled = PAIR == kPairBlock || PAIR == kPairBlockK || PAIR == kPairBlockE8;
+  constexpr bool kPromote = PAIR == kPairBlock || PAIR == kPairBlockK;
+  constexpr bool kWeightBlocks = PAIR == kPairBlock || PAIR == kPairBlockE8;  // B scales per 128 x 128
   // per-step scale vectors of the blockwise pairs, staged like the tiles:
   // A row scales (BM floats) and B scales (the BN/128 weight-block scales,
   // or BN column scales for 1x128 x 1x128)
   constexpr int kScaleA = kBlockScaled ? BM * 4 : 0;
-  constexpr int kScaleB = PAIR == kPairBlockK ? BN * 4 : (PAIR == kPairBlock ? 256 : 0);
+  constexpr int kScaleB = PAIR == kPairBlockK ? BN * 4 : (kWeightBlocks ? 256 : 0);
   constexpr int kScaleStage = kScaleA + kScaleB;
   // LDS ring of kStages operand stages (and their scale vectors): the loads
   // of stage kt + kStages - 1 go out during step kt.  The 256 x 256 tile
@@ -370,7 +389,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       q_base = (int)m0 * 4;
     } else if (wave < kQ) {
       q_dst = kScaleA + (wave - kQA) * 256;
-      if (PAIR == kPairBlock) {
+      if (kWeightBlocks) {
         // the tile's BN / 128 weight blocks, each with K / 128 scales
         q_voff = lane < (BN + 127) / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
         q_ld = 4;
@@ -545,6 +564,15 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
     // product below), which the reads' addresses depend on.
     const v8i none = {};
     const FragAddr fa = frag_addr(cur + wm * 128), fb = frag_addr(cur + kTileA + wn * 128);
+    // power-of-two scales enter strip 0's MFMAs: read its row scale and the
+    // weight block's scale before the fragments, so the first fragment wait
+    // covers them; the row scales of later strips follow strip by strip
+    const uint32_t sa_addr = lds_addr(cur_scales) + (wm + (lane & 15)) * 4;
+    float sa_e[TI], sb_e = 0.f;
+    if constexpr (PAIR == kPairBlockE8) {
+      sb_e = lds_read_f32(lds_addr(cur_scales + kScaleA) + (wn / 128) * 4, 0);
+      sa_e[0] = lds_read_f32(sa_addr, 0);
+    }
     v8i af = read_frag<0>(fa, none, none, done);
     v8i bf[TJ];
     static_for<TJ>([&](auto j) { bf[j] = read_frag<j * 2048>(fb, none, none, done); });
@@ -588,21 +616,37 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       }
     };
 
-    if constexpr (!kBlockScaled) {
+    if constexpr (!kPromote) {
       // Whole-K accumulation in the MFMA accumulator.  Strip i multiplies
       // with af; the fragment of strip i+2 is read into registers that are
       // neither af nor af_next (early clobber against them via `busy`) once
       // the MFMAs of strip i-1 are done (their output is multiplied into
       // `done` first), so it never overwrites a source still being read.
+      // With power-of-two scales, strip i+1's row scale is read just before
+      // that fragment, so the same wait covers it.
+      int se_b = 0;
       static_for<TI>([&](auto ic) {
         constexpr int i = decltype(ic)::value;
+        int se_a = 0;
         static_for<TJ>([&](auto jc) {
           constexpr int j = decltype(jc)::value;
-          if constexpr (i == 0) wait_b(jc);
-          acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
+          if constexpr (i == 0) {
+            wait_b(jc);
+            if constexpr (PAIR == kPairBlockE8 && j == 0) {
+              asm volatile("" : "+v"(sb_e), "+v"(sa_e[0]));
+              se_b = e8m0_of(sb_e);
+            }
+          }
+          if constexpr (PAIR == kPairBlockE8) {
+            if constexpr (j == 0) se_a = e8m0_of(sa_e[i]);
+            acc[i][j] = mfma_16x16x128_e8(bf[j], af, acc[i][j], se_b, se_a);
+          } else {
+            acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
+          }
           after_mfma(ic, jc);
         });
         if constexpr (i == 0) mid_barrier();
+        if constexpr (PAIR == kPairBlockE8 && i + 1 < TI) sa_e[i + 1] = lds_read_f32(sa_addr, (i + 1) * 64);
         v8i af_after = af_next;
         if constexpr (i + 2 < TI) {
           if constexpr (i > 0) done = acc[i - 1][TJ - 1][3] * 0.0f;
@@ -611,6 +655,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
         } else if constexpr (i + 1 < TI) {
           lds_wait<0>(af_next);  // the last fragment
         }
+        if constexpr (PAIR == kPairBlockE8 && i + 1 < TI) asm volatile("" : "+v"(sa_e[i + 1]));
         af = af_next;
         af_next = af_after;
       });
@@ -840,7 +885,7 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
       int64_t da = 0, db = 0;
       if (PAIR != kPairTensor) da = m;
       if (PAIR == kPairRow || PAIR == kPairBlockK) db = n;
-      if (PAIR == kPairBlock) db = (n / 128) * (g.K / 128);
+      if (PAIR == kPairBlock || PAIR == kPairBlockE8) db = (n / 128) * (g.K / 128);
       sub.sA = g.sA + da;
       sub.sB = g.sB + db;
       sub.sa_count = g.sa_count - da;
@@ -867,6 +912,9 @@ FP8Q_GEMM_KERNEL(kPairTensor, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairRow, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairBlock, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairBlockK, 64, 64, 32, 32)
+FP8Q_GEMM_KERNEL(kPairBlockE8, 256, 256, 128, 64)
+FP8Q_GEMM_KERNEL(kPairBlockE8, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL(kPairBlockE8, 64, 64, 32, 32)
 #undef FP8Q_GEMM_KERNEL
 template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true>(GemmArgs);
 template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true>(GemmArgs);
@@ -881,6 +929,7 @@ hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s) {
     case kPairRow: return launch_split<kPairRow, false>(g, s);
     case kPairBlock: return launch_split<kPairBlock, false>(g, s);
     case kPairBlockK: return launch_split<kPairBlockK, false>(g, s);
+    case kPairBlockE8: return launch_split<kPairBlockE8, false>(g, s);
     default: return hipErrorInvalidValue;
   }
 }

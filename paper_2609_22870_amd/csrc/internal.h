@@ -14,6 +14,7 @@ struct QuantArgs {
   uint8_t* codes;     // [rows][ldc] or [cols][ldc] when transposed
   int64_t ldc;
   float* scales;
+  int pow2;           // power-of-two scales (FP8Q_POW2_SCALE)
 };
 
 // granularity: the fp8q_granularity value; nscales: entries of `scales`.
@@ -55,7 +56,9 @@ struct GemmArgs {
   int64_t ldq, cs_ld;
 };
 
-enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3 };
+// kPairBlockE8: 1x128 x 128x128 with power-of-two scales (applied inside
+// the matrix instruction)
+enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3, kPairBlockE8 = 4 };
 
 hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s);
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s);

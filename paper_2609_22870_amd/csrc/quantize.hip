@@ -142,9 +142,10 @@ __device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8]
 // 16 lanes of its DPP row: lane cc of the row group holds the amax of row
 // cc % 8, computes that unit's S and 1/S (two IEEE divisions), and the
 // group exchanges them by lane shuffles.
-__device__ __forceinline__ void share_row_units(float amax, UnitScale& mine, float (&su)[8], float (&ru)[8]) {
+__device__ __forceinline__ void share_row_units(float amax, bool pow2, UnitScale& mine, float (&su)[8],
+                                                float (&ru)[8]) {
   const int lane = threadIdx.x & 63;
-  mine = unit_scale(amax);
+  mine = unit_scale(amax, pow2);
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     su[i] = __shfl(mine.s, (lane & 48) | i, 64);
@@ -156,10 +157,10 @@ __device__ __forceinline__ void share_row_units(float amax, UnitScale& mine, flo
 // (rg < 8, cc) holds the amax of column 8 cc + rg, computes its S and 1/S,
 // and the block exchanges them through LDS (the upper half of lds_red, after
 // every read of its lower half).
-__device__ __forceinline__ void share_col_units(float amax, float* lds_red, UnitScale& mine, float (&su)[8],
-                                                float (&ru)[8]) {
+__device__ __forceinline__ void share_col_units(float amax, bool pow2, float* lds_red, UnitScale& mine,
+                                                float (&su)[8], float (&ru)[8]) {
   const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  mine = unit_scale(amax);
+  mine = unit_scale(amax, pow2);
   float2* lds_su = reinterpret_cast<float2*>(lds_red + 2 * kTile);
   __syncthreads();
   if (rg < 8) lds_su[cc * 8 + rg] = make_float2(mine.s, mine.r);
@@ -275,7 +276,7 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       const int64_t r = row0 + (cc & 7);
       amax = r < a.rows ? a.scales[r] : 0.0f;
     }
-    share_row_units(amax, mine, su, ru);
+    share_row_units(amax, a.pow2 != 0, mine, su, ru);
   } else if (by_col) {
     float amax;
     if (K == kBlock128x1) {
@@ -288,9 +289,9 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       const int64_t cj = c0 + cc * 8 + (rg & 7);
       amax = cj < a.cols ? a.scales[cj] : 0.0f;
     }
-    share_col_units(amax, lds_red, mine, su, ru);
+    share_col_units(amax, a.pow2 != 0, lds_red, mine, su, ru);
   } else {
-    mine = unit_scale(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0]);
+    mine = unit_scale(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0], a.pow2 != 0);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       su[i] = mine.s;
@@ -346,7 +347,7 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
   UnitScale mine;
   float su[8], ru[8];
 
-  share_row_units(block_row_amax(t), mine, su, ru);
+  share_row_units(block_row_amax(t), a.pow2 != 0, mine, su, ru);
   encode_patch<kUnitRow>(t, su, ru, packed);
   store_patch(packed, a.codes, a.ldc, a.rows, a.cols, row0, c);
   {
@@ -359,7 +360,7 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
   float amax = m[0];
 #pragma unroll
   for (int j = 1; j < 8; ++j) amax = (rg & 7) == j ? m[j] : amax;
-  share_col_units(amax, lds_red, mine, su, ru);
+  share_col_units(amax, a.pow2 != 0, lds_red, mine, su, ru);
   encode_patch<kUnitCol>(t, su, ru, packed);
   store_patch_transposed(packed, lds_t, d.codes_t, d.ldc_t, a.rows, a.cols, r0, c0);
   const int64_t cj = c0 + cc * 8 + rg;
@@ -442,7 +443,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) 
 #pragma unroll
       for (int q = 0; q < 8; ++q) m = fmaxf(m, row_partial_max(t, q));
     }
-    const UnitScale u = unit_scale(wave_max(m));
+    const UnitScale u = unit_scale(wave_max(m), a.pow2 != 0);
     float su[8], ru[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -493,9 +494,9 @@ __global__ void fill_zero_kernel(float* p, int64_t n) {
     p[i] = 0.0f;
 }
 
-__global__ void amax_to_scale_kernel(float* p, int64_t n) {
+__global__ void amax_to_scale_kernel(float* p, int64_t n, int pow2) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = unit_scale(p[i]).s;
+    p[i] = unit_scale(p[i], pow2 != 0).s;
 }
 
 __global__ void cast_f32_kernel(const float* x, int64_t n, float scale, uint8_t* codes) {
@@ -530,7 +531,7 @@ hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipS
   if ((e = hipGetLastError()) != hipSuccess) return e;
   e = trans ? launch_tile<K, true>(a, s) : launch_tile<K, false>(a, s);
   if (e != hipSuccess) return e;
-  amax_to_scale_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales);
+  amax_to_scale_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales, a.pow2);
   return hipGetLastError();
 }
 

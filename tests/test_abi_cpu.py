@@ -77,7 +77,7 @@ def test_quantize_rejections(L):
     assert quant(L, rows=0) == -1
     assert quant(L, cols=-5) == -1
     assert quant(L, g=6) == -1
-    assert quant(L, flags=2) == -1
+    assert quant(L, flags=4) == -1                           # unknown flag bit
     assert quant(L, ldx=128) == -1
     assert quant(L, ldc=128) == -1
     assert quant(L, cols=200, ldx=200, ldc=208) == -2        # cols % 16
@@ -114,6 +114,28 @@ def test_gemm_rejections(L):
     assert gemm(L, lda=264) == -3
     assert gemm(L, C=FAKE + 2) == -3
     assert gemm(L, ldc=258) == -3
+
+
+def test_gemm_pow2_rejections(L):
+    def gp(**kw):
+        args = dict(A=FAKE, sA=FAKE, gA=3, lda=256, B=FAKE, sB=FAKE, gB=5, ldb=256, M=256, N=256, K=256,
+                    C=FAKE, ldc=256)
+        args.update(kw)
+        return L.fp8q_gemm_pow2(*args.values(), None)
+    assert gp(A=None) == -1
+    assert gp(M=0) == -1
+    assert gp(gA=0, gB=0) == -2                              # only 1x128 x 128x128
+    assert gp(gA=3, gB=3) == -2
+    assert gp(N=200, ldc=256) == -2
+    assert gp(K=200) == -2
+    assert gp(A=FAKE + 4) == -3
+    assert gp(ldc=258) == -3
+
+
+def test_scales_count_pow2_flag(L):
+    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 2) == 256 * 3
+    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 3) == 256 * 3
+    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 4) == -1
 
 
 def test_cast_rejections(L):
