@@ -21,6 +21,10 @@
  *   - Q_FP8 rounds that fp32 quotient to nearest, ties to even mantissa,
  *     and clamps magnitudes above 448 to 448.  The sign of zero is kept.
  *   - fp32 subnormals are kept (no flush to zero).
+ * Variants offered next to the paper's method (flags of oracle_quantize):
+ *   - ORACLE_E5M2: the format is OCP E5M2, F_max = 57344 (for gradients).
+ *   - ORACLE_POW2_SCALE: S is the smallest power of two with F_max S >= amax,
+ *     at least 2^-127, and 1 when amax is 0.
  *
  * Scale layouts (fp32, "rows" and "cols" are those of the OUTPUT matrix,
  * which is the input matrix or, with ORACLE_OUT_TRANSPOSED, its transpose):
@@ -53,7 +57,9 @@ enum {
   ORACLE_BLOCK_128x1 = 4,
   ORACLE_BLOCK_128x128 = 5
 };
-enum { ORACLE_OUT_TRANSPOSED = 1, ORACLE_POW2_SCALE = 2 };
+enum { ORACLE_OUT_TRANSPOSED = 1, ORACLE_POW2_SCALE = 2, ORACLE_E5M2 = 4 };
+/* Operand formats of oracle_gemm_rows_fmt. */
+enum { ORACLE_FMT_E4M3 = 0, ORACLE_FMT_E5M2 = 1 };
 
 /* Value of an OCP E4M3 byte; NaN for 0x7F and 0xFF. */
 double oracle_e4m3_decode(uint8_t code);
@@ -62,6 +68,14 @@ double oracle_e4m3_decode(uint8_t code);
  * magnitudes >= 448 clamp to 448, sign kept (also for zero).
  * NaN input returns 0x7F (never produced for finite input). */
 uint8_t oracle_e4m3_encode(float v);
+
+/* Value of an OCP E5M2 byte: +-inf for 0x7C / 0xFC, NaN for 0x7D..0x7F and
+ * 0xFD..0xFF. */
+double oracle_e5m2_decode(uint8_t code);
+
+/* Q_FP8 into E5M2: nearest E5M2 value, ties to even mantissa, magnitudes
+ * >= 57344 clamp to 57344 (never infinity), sign kept.  NaN returns 0x7F. */
+uint8_t oracle_e5m2_encode(float v);
 
 /* Eq. 3 applied per scaling unit.  x_bf16 is row-major [rows][ldx] bf16
  * bit patterns; codes is [rows][ldc] (or [cols][ldc] when transposed).
@@ -75,6 +89,9 @@ uint8_t oracle_cast_f32(float x, float scale);
 /* Same over an array; used to check the device cast routine. */
 void oracle_cast_f32_array(const float *x, int64_t n, float scale,
                            uint8_t *codes);
+/* The E5M2 form: oracle_e5m2_encode(RN32(x[i] / scale)). */
+void oracle_cast_f32_e5m2_array(const float *x, int64_t n, float scale,
+                                uint8_t *codes);
 
 /* Exact product of the dequantized operands of the FP8 linear layer:
  *   C[m][n] = sum_k (S_A(m,k) * A_hat[m][k]) * (S_B(n,k) * B_hat[n][k])
@@ -89,6 +106,13 @@ int oracle_gemm_rows(const uint8_t *A, const float *sA, int gA, int64_t lda,
                      const uint8_t *B, const float *sB, int gB, int64_t ldb,
                      int64_t M, int64_t N, int64_t K, const int64_t *rows,
                      int64_t nrows, double *out);
+/* The same with the codes of A and of B each in E4M3 or E5M2
+ * (ORACLE_FMT_*). */
+int oracle_gemm_rows_fmt(const uint8_t *A, const float *sA, int gA,
+                         int64_t lda, int fmtA, const uint8_t *B,
+                         const float *sB, int gB, int64_t ldb, int fmtB,
+                         int64_t M, int64_t N, int64_t K, const int64_t *rows,
+                         int64_t nrows, double *out);
 
 #ifdef __cplusplus
 }

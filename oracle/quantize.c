@@ -9,6 +9,9 @@
  * Tensorwise, rowwise and blockwise units follow the paragraph on scaling
  * granularity in Sec. 2.2; the 1x128 / 128x1 / 128x128 block shapes are the
  * ones the FP8 linear layer uses for activations, wgrad operands and weights.
+ *
+ * With ORACLE_E5M2 the FP8 format is E5M2 instead: F_max = 57344 replaces
+ * 448 in the scale and the codes are E5M2 (oracle_e5m2_encode).
  */
 #include <math.h>
 #include <stdlib.h>
@@ -61,20 +64,21 @@ static int64_t scale_index(int g, int64_t rows, int64_t cols, int64_t r,
   }
 }
 
-static float scale_from_amax(float amax) {
-  float s = amax / 448.0f; /* one correctly rounded fp32 division */
+/* F_max is 448 (E4M3) or 57344 (E5M2); both are exact in fp32. */
+static float scale_from_amax(float amax, float fmax) {
+  float s = amax / fmax; /* one correctly rounded fp32 division */
   if (s == 0.0f) s = 1.0f;
   return s;
 }
 
 /* The power-of-two variant (not the paper's scale): the smallest power of
- * two S with 448 S >= amax, at least 2^-127, and 1 for amax = 0.  Found by
- * exact comparisons of 448 * 2^k with amax in double. */
-static float pow2_scale_from_amax(float amax) {
+ * two S with F_max S >= amax, at least 2^-127, and 1 for amax = 0.  Found
+ * by exact comparisons of F_max * 2^k with amax in double. */
+static float pow2_scale_from_amax(float amax, float fmax) {
   if (amax == 0.0f) return 1.0f;
-  int k = ilogb(amax) - 8;
-  while (ldexp(448.0, k) < (double)amax) ++k;
-  while (ldexp(448.0, k - 1) >= (double)amax) --k;
+  int k = ilogb(amax) - ilogb(fmax);
+  while (ldexp((double)fmax, k) < (double)amax) ++k;
+  while (ldexp((double)fmax, k - 1) >= (double)amax) --k;
   if (k < -127) k = -127;
   return (float)ldexp(1.0, k);
 }
@@ -87,6 +91,11 @@ uint8_t oracle_cast_f32(float x, float scale) {
 void oracle_cast_f32_array(const float *x, int64_t n, float scale,
                            uint8_t *codes) {
   for (int64_t i = 0; i < n; ++i) codes[i] = oracle_cast_f32(x[i], scale);
+}
+
+void oracle_cast_f32_e5m2_array(const float *x, int64_t n, float scale,
+                                uint8_t *codes) {
+  for (int64_t i = 0; i < n; ++i) codes[i] = oracle_e5m2_encode(x[i] / scale);
 }
 
 int oracle_quantize(const uint16_t *x_bf16, int64_t rows, int64_t cols,
@@ -123,15 +132,19 @@ int oracle_quantize(const uint16_t *x_bf16, int64_t rows, int64_t cols,
   }
   /* S of every unit */
   int pow2 = (flags & ORACLE_POW2_SCALE) != 0;
+  int e5m2 = (flags & ORACLE_E5M2) != 0;
+  float fmax = e5m2 ? 57344.0f : 448.0f;
   for (int64_t u = 0; u < nunits; ++u)
-    scales[u] = pow2 ? pow2_scale_from_amax(amax[u]) : scale_from_amax(amax[u]);
+    scales[u] = pow2 ? pow2_scale_from_amax(amax[u], fmax)
+                     : scale_from_amax(amax[u], fmax);
   /* codes */
   for (int64_t r = 0; r < rows; ++r) {
     for (int64_t c = 0; c < cols; ++c) {
       float x = bf16_to_float(x_bf16[r * ldx + c]);
       int64_t orr = transposed ? c : r, occ = transposed ? r : c;
       int64_t u = scale_index(og, orows, ocols, orr, occ);
-      codes[orr * ldc + occ] = oracle_e4m3_encode(x / scales[u]);
+      float q = x / scales[u]; /* one correctly rounded fp32 division */
+      codes[orr * ldc + occ] = e5m2 ? oracle_e5m2_encode(q) : oracle_e4m3_encode(q);
     }
   }
   free(amax);

@@ -2,9 +2,10 @@
  * Test helper: checks the quotient sequence the HIP quantizer uses for
  * RN32(x / S) against the correctly rounded division, over every pair of a
  * positive finite bf16 amax and a bf16 x with |x| <= amax (both signs, both
- * zeros), and reports the pairs whose E4M3 code (sign included) differs.
+ * zeros), and reports the pairs whose E4M3 code (sign included) differs;
+ * div_sweep_fmt does the same for E5M2 codes, with F_max = 57344.
  *
- * Kernel sequence, for S = RN32(amax / 448) (1 if 0) and r = RN32(1 / S):
+ * Kernel sequence, for S = RN32(amax / F_max) (1 if 0) and r = RN32(1 / S):
  *   q0 = RN(x r);  e = RN(q0 S - x) (one FMA);  q = RN(q0 - e r) (one FMA)
  * used when S >= 2^-90; smaller S take the IEEE division.  Host fmaf and
  * float multiply are the same IEEE operations as v_fma_f32 / v_mul_f32
@@ -32,13 +33,29 @@ static uint32_t code_of(float v) {
   return s | (q < 8.0 ? (uint32_t)q : (uint32_t)(((E + 7) << 3) | ((int)q - 8)));
 }
 
-struct job { uint32_t a_lo, a_hi; uint64_t pairs, bad; uint32_t bad_a, bad_x; };
+/* E5M2 code of an fp32 value, written from the format (sign, RNE, clamp
+ * at 57344): 2 mantissa bits, normal binades from 2^-14, subnormal grid
+ * 2^-16. */
+static uint32_t code_of_e5m2(float v) {
+  uint32_t s = signbit(v) ? 0x80u : 0u;
+  double a = fabs((double)v);
+  if (a >= 57344.0) return s | 0x7Bu;
+  int e2;
+  (void)frexp(a, &e2);
+  int E = (a == 0.0) ? -14 : e2 - 1;
+  if (E < -14) E = -14;
+  double q = nearbyint(ldexp(a, 2 - E));
+  if (q >= 8.0) { q = 4.0; E += 1; }
+  return s | (q < 4.0 ? (uint32_t)q : (uint32_t)(((E + 15) << 2) | ((int)q - 4)));
+}
+
+struct job { uint32_t a_lo, a_hi; int e5m2; uint64_t pairs, bad; uint32_t bad_a, bad_x; };
 
 static void *worker(void *p) {
   struct job *j = (struct job *)p;
   for (uint32_t ai = j->a_lo; ai < j->a_hi; ++ai) {
     float amax = f32(ai << 16);
-    float S = amax / 448.0f;
+    float S = amax / (j->e5m2 ? 57344.0f : 448.0f);
     if (S == 0.0f) S = 1.0f;
     float r = 1.0f / S;
     int fast = S >= 0x1p-90f;
@@ -55,7 +72,9 @@ static void *worker(void *p) {
           q = x / S;
         }
         ++j->pairs;
-        if (code_of(q) != code_of(exact)) {
+        uint32_t cq = j->e5m2 ? code_of_e5m2(q) : code_of(q);
+        uint32_t ce = j->e5m2 ? code_of_e5m2(exact) : code_of(exact);
+        if (cq != ce) {
           if (!j->bad) { j->bad_a = ai; j->bad_x = xi | sign; }
           ++j->bad;
         }
@@ -65,8 +84,9 @@ static void *worker(void *p) {
   return 0;
 }
 
-/* Returns the number of differing pairs; *pairs gets the count checked. */
-uint64_t div_sweep(int threads, uint64_t *pairs, uint32_t *bad_a, uint32_t *bad_x) {
+/* Returns the number of differing pairs; *pairs gets the count checked.
+ * e5m2 selects the E5M2 codes and F_max. */
+uint64_t div_sweep_fmt(int threads, int e5m2, uint64_t *pairs, uint32_t *bad_a, uint32_t *bad_x) {
   if (threads < 1) threads = 1;
   if (threads > 64) threads = 64;
   pthread_t tid[64];
@@ -80,7 +100,7 @@ uint64_t div_sweep(int threads, uint64_t *pairs, uint32_t *bad_a, uint32_t *bad_
     uint32_t hi = (t == threads - 1) ? 0x7F80u : (uint32_t)sqrt(2.0 * target);
     if (hi < lo) hi = lo;
     if (hi > 0x7F80u) hi = 0x7F80u;
-    jobs[t] = (struct job){lo, hi, 0, 0, 0, 0};
+    jobs[t] = (struct job){lo, hi, e5m2, 0, 0, 0, 0};
     pthread_create(&tid[t], 0, worker, &jobs[t]);
     lo = hi;
   }
@@ -94,4 +114,8 @@ uint64_t div_sweep(int threads, uint64_t *pairs, uint32_t *bad_a, uint32_t *bad_
   }
   *pairs = n;
   return bad;
+}
+
+uint64_t div_sweep(int threads, uint64_t *pairs, uint32_t *bad_a, uint32_t *bad_x) {
+  return div_sweep_fmt(threads, 0, pairs, bad_a, bad_x);
 }
