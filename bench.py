@@ -151,7 +151,10 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
       float32 arrays), both of its kernels;
     * the step's GEMM on operands quantized with power-of-two scales (a
       variant, not the paper's scale), whose block scales enter the matrix
-      instruction, with that quantization of X."""
+      instruction, with that quantization of X;
+    * the E5M2 variant for gradients on the same dY: its dual-layout
+      quantization, and the 32B up-projection's data-gradient GEMM dX = dY W
+      (16384 x 25600 -> 5120) with dY's codes in E5M2 against E4M3."""
     rows, cols = 16384, 25600
     dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
     outs = fp8q.quantize_dual(dy)
@@ -175,7 +178,20 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
                            fp8q.quantize(dy, fp8q.BLOCK_128x1, transposed=True, codes=r2[0], scales=r2[1])))
     nbytes = 4.0 * rows * cols + 4.0 * (outs[1].numel() + outs[3].numel())
     gbs = nbytes / (t_dual * 1e-6) / 1e9
-    del dy, outs, r1, r2
+    del r1, r2
+
+    k_in = 5120
+    w32 = synth.weights(cols, k_in, seed=synth.seed_for(5, 1), device=dev)
+    wt, swt = fp8q.quantize(w32, fp8q.BLOCK_128x128, transposed=True)    # W^T [5120, 25600]
+    del w32
+    outs5 = fp8q.quantize_dual(dy, e5m2=True)
+    t_dual5 = timed(lambda: fp8q.quantize_dual(dy, *outs5, e5m2=True))
+    dx = torch.empty((rows, k_in), dtype=torch.bfloat16, device=dev)
+    t_dg4 = timed(lambda: fp8q.gemm(outs[0], outs[1], fp8q.BLOCK_1x128, wt, swt, fp8q.BLOCK_128x128, out=dx))
+    t_dg5 = timed(lambda: fp8q.gemm_formats(outs5[0], outs5[1], fp8q.BLOCK_1x128, wt, swt, fp8q.BLOCK_128x128,
+                                            fp8q.A_E5M2, out=dx))
+    dg_flops = 2.0 * rows * cols * k_in
+    del dy, outs, outs5, wt, swt, dx
 
     M, N, K = xq.shape[0], wq.shape[0], xq.shape[1]
     y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
@@ -216,6 +232,10 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
         "gemm_pow2_scales_8b_ffn_up": {
         "shape": [M, K, N], "us": round(t_pow2, 1), "tflops": round(pow2_tflops, 1),
         "frac_mfma": round(pow2_tflops / PEAK_FP8_TFLOPS, 4), "quantize_x_pow2_us": round(t_qx2, 1)},
+        "e5m2_dy_32b_up": {
+        "dual_quantize_us": round(t_dual5, 1), "dgrad_shape": [rows, cols, k_in],
+        "dgrad_e5m2_us": round(t_dg5, 1), "dgrad_e5m2_tflops": round(dg_flops / (t_dg5 * 1e-6) / 1e12, 1),
+        "dgrad_e4m3_us": round(t_dg4, 1), "dgrad_e4m3_tflops": round(dg_flops / (t_dg4 * 1e-6) / 1e12, 1)},
         "calibrated_clipping_grpo_batch": {
         "tokens": ntok, "us": round(t_clip, 1), "gbs": round(clip_gbs, 1),
         "frac_hbm": round(clip_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": round(clip_bytes)}}

@@ -68,6 +68,12 @@ enum { FP8Q_OUT_TRANSPOSED = 1u };
  * amax is 0.  Every |x| / S is then at most 448 and exact, and S fits the
  * E8M0 block scales of the MI355X matrix instructions. */
 enum { FP8Q_POW2_SCALE = 2u };
+/* E5M2 codes instead of E4M3 (a variant for gradients; the paper leaves
+ * the FP8 format of Eq. 3 open): OCP E5M2, F_max = 57344, so S =
+ * RN32(amax / 57344) and each code is the nearest-even E5M2 value of
+ * RN32(x / S) clamped at 57344 (never an infinity).  With FP8Q_POW2_SCALE,
+ * S is the smallest power of two with 57344 S >= amax, at least 2^-127. */
+enum { FP8Q_E5M2 = 4u };
 
 /*
  * Number of fp32 scales fp8q_quantize writes for an input of rows x cols
@@ -91,10 +97,11 @@ int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g,
                           unsigned flags);
 
 /*
- * Eq. 3 per scaling unit: codes and scales of x.  flags: FP8Q_OUT_TRANSPOSED,
- * FP8Q_POW2_SCALE, or both.
+ * Eq. 3 per scaling unit: codes and scales of x.  flags: any of
+ * FP8Q_OUT_TRANSPOSED, FP8Q_POW2_SCALE and FP8Q_E5M2.
  *   x       bf16 [rows][ldx], ldx >= cols
- *   codes   E4M3 [rows][ldc] (ldc >= cols), or [cols][ldc] (ldc >= rows)
+ *   codes   E4M3 (E5M2 with FP8Q_E5M2) [rows][ldc] (ldc >= cols), or
+ *           [cols][ldc] (ldc >= rows)
  *           with FP8Q_OUT_TRANSPOSED
  *   scales  fp32, fp8q_scales_count(rows, cols, g, flags) entries
  * Shape rules: cols % 16 == 0, and rows % 16 == 0 when transposed; a
@@ -115,22 +122,23 @@ fp8q_status fp8q_quantize(const void *x, int64_t rows, int64_t cols,
  * token dimension, so it takes x (an activation X or an output gradient dY)
  * transposed and grouped by 128 along the rows, while the forward and
  * data-gradient GEMMs take it grouped by 128 along the columns.  Outputs:
- *   codes_r, scales_r  exactly fp8q_quantize(x, FP8Q_BLOCK_1x128, 0):
+ *   codes_r, scales_r  exactly fp8q_quantize(x, FP8Q_BLOCK_1x128, flags):
  *                      codes [rows][ldc_r] (ldc_r >= cols), scales
  *                      [cols/128][rows]
  *   codes_t, scales_t  exactly fp8q_quantize(x, FP8Q_BLOCK_128x1,
- *                      FP8Q_OUT_TRANSPOSED): codes [cols][ldc_t] (ldc_t >=
- *                      rows), scales [rows/128][cols]
- * x is bf16 [rows][ldx].  Shape rules: rows % 128 == 0 and cols % 128 == 0
+ *                      FP8Q_OUT_TRANSPOSED | flags): codes [cols][ldc_t]
+ *                      (ldc_t >= rows), scales [rows/128][cols]
+ * x is bf16 [rows][ldx].  flags: FP8Q_POW2_SCALE, FP8Q_E5M2 (for an output
+ * gradient), both, or 0; any other bit is FP8Q_ERR_INVAL.  Shape rules: rows % 128 == 0 and cols % 128 == 0
  * (else FP8Q_ERR_UNSUPPORTED).  Alignment: x and both code arrays 16-byte
  * aligned, ldx % 8 == 0, ldc_r % 16 == 0, ldc_t % 16 == 0, scales 4-byte
  * aligned (else FP8Q_ERR_ALIGN).  The four outputs must not overlap.
  */
 fp8q_status fp8q_quantize_dual(const void *x, int64_t rows, int64_t cols,
-                               int64_t ldx, uint8_t *codes_r, int64_t ldc_r,
-                               float *scales_r, uint8_t *codes_t,
-                               int64_t ldc_t, float *scales_t,
-                               struct ihipStream_t *stream);
+                               int64_t ldx, unsigned flags, uint8_t *codes_r,
+                               int64_t ldc_r, float *scales_r,
+                               uint8_t *codes_t, int64_t ldc_t,
+                               float *scales_t, struct ihipStream_t *stream);
 
 /*
  * The FP8 linear layer's GEMM on dequantized operands (Eq. 3 applied to
@@ -155,6 +163,25 @@ fp8q_status fp8q_gemm(const uint8_t *A, const float *sA, fp8q_granularity gA,
                       fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N,
                       int64_t K, void *C, int64_t ldc,
                       struct ihipStream_t *stream);
+
+/* Operand formats of fp8q_gemm_formats: A's codes, B's codes are E5M2. */
+enum { FP8Q_A_E5M2 = 1u, FP8Q_B_E5M2 = 2u };
+
+/*
+ * fp8q_gemm with each operand's codes in E4M3 or E5M2 (the E5M2 variant of
+ * FP8Q_E5M2, for output gradients): `formats` is 0 or FP8Q_A_E5M2,
+ * FP8Q_B_E5M2, or both; any other bit is FP8Q_ERR_INVAL.  The product,
+ * layouts, shape and alignment rules are those of fp8q_gemm.  Non-zero
+ * formats are supported for the backward pairs (1x128, 128x128) — dgrad
+ * dX = dY W with dY in E5M2 — and (1x128, 1x128) — wgrad dW = dY^T X —
+ * (else FP8Q_ERR_UNSUPPORTED); formats 0 is fp8q_gemm.
+ */
+fp8q_status fp8q_gemm_formats(const uint8_t *A, const float *sA,
+                              fp8q_granularity gA, int64_t lda,
+                              const uint8_t *B, const float *sB,
+                              fp8q_granularity gB, int64_t ldb, int64_t M,
+                              int64_t N, int64_t K, unsigned formats, void *C,
+                              int64_t ldc, struct ihipStream_t *stream);
 
 /*
  * fp8q_gemm for operands quantized with FP8Q_POW2_SCALE: the same product
@@ -262,6 +289,9 @@ fp8q_status fp8q_calibrate_clip(const float *adv, const float *w_tis,
  */
 fp8q_status fp8q_cast_f32(const float *x, int64_t n, float scale,
                           uint8_t *codes, struct ihipStream_t *stream);
+/* The same with the E5M2 codes of FP8Q_E5M2 (clamp at 57344). */
+fp8q_status fp8q_cast_f32_e5m2(const float *x, int64_t n, float scale,
+                               uint8_t *codes, struct ihipStream_t *stream);
 
 /* Static string naming a status. */
 const char *fp8q_status_string(fp8q_status status);

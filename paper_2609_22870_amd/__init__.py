@@ -19,12 +19,15 @@ LIB_PATH = os.path.join(_HERE, "libfp8q.so")
 TENSOR, ROW, COL, BLOCK_1x128, BLOCK_128x1, BLOCK_128x128 = range(6)
 OUT_TRANSPOSED = 1
 POW2_SCALE = 2
+E5M2 = 4                      # quantize flag: E5M2 codes (F_max = 57344)
+A_E5M2, B_E5M2 = 1, 2         # gemm_formats operand formats
 _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
            -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
-           "fp8q_gemm", "fp8q_gemm_pow2", "fp8q_gemm_quantized", "fp8q_calibrate_clip_workspace",
-           "fp8q_calibrate_clip", "fp8q_cast_f32", "fp8q_status_string")
+           "fp8q_gemm", "fp8q_gemm_formats", "fp8q_gemm_pow2", "fp8q_gemm_quantized",
+           "fp8q_calibrate_clip_workspace", "fp8q_calibrate_clip", "fp8q_cast_f32",
+           "fp8q_cast_f32_e5m2", "fp8q_status_string")
 
 
 class ClipConfig(ctypes.Structure):
@@ -68,11 +71,13 @@ def lib():
         L.fp8q_scales_count.restype = i64
         L.fp8q_quantize.argtypes = [p, i64, i64, i64, i32, u32, p, i64, p, p]
         L.fp8q_quantize.restype = i32
-        L.fp8q_quantize_dual.argtypes = [p, i64, i64, i64, p, i64, p, p, i64, p, p]
+        L.fp8q_quantize_dual.argtypes = [p, i64, i64, i64, u32, p, i64, p, p, i64, p, p]
         L.fp8q_quantize_dual.restype = i32
         L.fp8q_gemm.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
                                 p, i64, p]
         L.fp8q_gemm.restype = i32
+        L.fp8q_gemm_formats.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64, u32, p, i64, p]
+        L.fp8q_gemm_formats.restype = i32
         L.fp8q_gemm_pow2.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64, p, i64, p]
         L.fp8q_gemm_pow2.restype = i32
         L.fp8q_gemm_quantized.argtypes = [p, p, i32, i64, p, p, i32, i64, i64,
@@ -85,6 +90,8 @@ def lib():
                                           p, i64, p, p]
         L.fp8q_calibrate_clip.restype = i32
         L.fp8q_cast_f32.argtypes = [p, i64, ctypes.c_float, p, p]
+        L.fp8q_cast_f32_e5m2.argtypes = [p, i64, ctypes.c_float, p, p]
+        L.fp8q_cast_f32_e5m2.restype = i32
         L.fp8q_cast_f32.restype = i32
         L.fp8q_status_string.argtypes = [i32]
         L.fp8q_status_string.restype = ctypes.c_char_p
@@ -116,19 +123,19 @@ def _ld(t):
 
 
 def scales_count(rows, cols, granularity, transposed=False):
-    n = lib().fp8q_scales_count(rows, cols, granularity,
-                                OUT_TRANSPOSED if transposed else 0)
+    n = lib().fp8q_scales_count(rows, cols, granularity, OUT_TRANSPOSED if transposed else 0)
     if n < 0:
         raise ValueError("invalid quantization shape or granularity")
     return n
 
 
-def quantize(x, granularity, transposed=False, codes=None, scales=None, pow2=False):
+def quantize(x, granularity, transposed=False, codes=None, scales=None, pow2=False, e5m2=False):
     """Eq. 3 per scaling unit on a bf16 CUDA tensor x[rows, cols].
 
     Returns (codes, scales): codes uint8 (OCP E4M3 bytes) [rows, cols], or
     [cols, rows] when `transposed`; scales fp32 1-D in the layout of
-    include/fp8q.h.  pow2: power-of-two scales (FP8Q_POW2_SCALE).
+    include/fp8q.h.  pow2: power-of-two scales (FP8Q_POW2_SCALE); e5m2:
+    E5M2 codes (FP8Q_E5M2).
     """
     if x.dtype != torch.bfloat16 or not x.is_cuda:
         raise ValueError("x must be a bf16 CUDA tensor")
@@ -140,17 +147,19 @@ def quantize(x, granularity, transposed=False, codes=None, scales=None, pow2=Fal
         scales = torch.empty(scales_count(rows, cols, granularity, transposed),
                              dtype=torch.float32, device=x.device)
     st = lib().fp8q_quantize(x.data_ptr(), rows, cols, _ld(x), granularity,
-                             (OUT_TRANSPOSED if transposed else 0) | (POW2_SCALE if pow2 else 0),
+                             (OUT_TRANSPOSED if transposed else 0) | (POW2_SCALE if pow2 else 0)
+                             | (E5M2 if e5m2 else 0),
                              codes.data_ptr(), _ld(codes), scales.data_ptr(),
                              _stream(x))
     _check(st, "fp8q_quantize")
     return codes, scales
 
 
-def quantize_dual(x, codes_r=None, scales_r=None, codes_t=None, scales_t=None):
+def quantize_dual(x, codes_r=None, scales_r=None, codes_t=None, scales_t=None, pow2=False, e5m2=False):
     """Both backward-pass layouts of a bf16 CUDA tensor x[rows, cols] from
     one read: (codes_r, scales_r) = quantize(x, BLOCK_1x128) and
-    (codes_t, scales_t) = quantize(x, BLOCK_128x1, transposed=True)."""
+    (codes_t, scales_t) = quantize(x, BLOCK_128x1, transposed=True), with
+    the same pow2 / e5m2 options."""
     if x.dtype != torch.bfloat16 or not x.is_cuda:
         raise ValueError("x must be a bf16 CUDA tensor")
     rows, cols = x.shape
@@ -165,6 +174,7 @@ def quantize_dual(x, codes_r=None, scales_r=None, codes_t=None, scales_t=None):
         scales_t = torch.empty(scales_count(rows, cols, BLOCK_128x1, True),
                                dtype=torch.float32, device=x.device)
     st = lib().fp8q_quantize_dual(x.data_ptr(), rows, cols, _ld(x),
+                                  (POW2_SCALE if pow2 else 0) | (E5M2 if e5m2 else 0),
                                   codes_r.data_ptr(), _ld(codes_r),
                                   scales_r.data_ptr(), codes_t.data_ptr(),
                                   _ld(codes_t), scales_t.data_ptr(), _stream(x))
@@ -188,6 +198,22 @@ def gemm(a, sa, ga, b, sb, gb, out=None):
                          b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                          out.data_ptr(), _ld(out), _stream(a))
     _check(st, "fp8q_gemm")
+    return out
+
+
+def gemm_formats(a, sa, ga, b, sb, gb, formats, out=None):
+    """gemm() with E5M2 codes for A (formats & A_E5M2) and/or B (formats &
+    B_E5M2): the backward pairs (1x128, 128x128) and (1x128, 1x128)."""
+    M, K = a.shape
+    N, K2 = b.shape
+    if K != K2:
+        raise ValueError("contraction sizes differ")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    st = lib().fp8q_gemm_formats(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
+                                 b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
+                                 formats, out.data_ptr(), _ld(out), _stream(a))
+    _check(st, "fp8q_gemm_formats")
     return out
 
 
@@ -260,13 +286,14 @@ def calibrate_clip(adv, w_tis, pi_sampler, r_bf16, r_fp8, l_old, h_old, config=N
     return {name: getattr(r, name) for name, _ in ClipResult._fields_}
 
 
-def cast_f32(x, scale, codes=None):
-    """Q_FP8(RN32(x / scale)) elementwise on an fp32 CUDA tensor."""
+def cast_f32(x, scale, codes=None, e5m2=False):
+    """Q_FP8(RN32(x / scale)) elementwise on an fp32 CUDA tensor (E4M3, or
+    E5M2 codes)."""
     if x.dtype != torch.float32 or not x.is_cuda or not x.is_contiguous():
         raise ValueError("x must be a contiguous fp32 CUDA tensor")
     if codes is None:
         codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
-    st = lib().fp8q_cast_f32(x.data_ptr(), x.numel(), float(scale),
-                             codes.data_ptr(), _stream(x))
-    _check(st, "fp8q_cast_f32")
+    fn = lib().fp8q_cast_f32_e5m2 if e5m2 else lib().fp8q_cast_f32
+    st = fn(x.data_ptr(), x.numel(), float(scale), codes.data_ptr(), _stream(x))
+    _check(st, "fp8q_cast_f32_e5m2" if e5m2 else "fp8q_cast_f32")
     return codes

@@ -12,6 +12,8 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 bool valid_granularity(int g) { return g >= FP8Q_TENSOR && g <= FP8Q_BLOCK_128x128; }
 
+constexpr unsigned kQuantFlags = FP8Q_OUT_TRANSPOSED | FP8Q_POW2_SCALE | FP8Q_E5M2;
+
 int transposed_granularity(int g) {
   switch (g) {
     case FP8Q_ROW: return FP8Q_COL;
@@ -56,75 +58,13 @@ bool grid_size(double lo, double hi, double step, int& n) {
   return true;
 }
 
-}  // namespace
-
-extern "C" {
-
-int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g, unsigned flags) {
-  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~(FP8Q_OUT_TRANSPOSED | FP8Q_POW2_SCALE)))
-    return -1;
-  const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
-  const int64_t orows = t ? cols : rows, ocols = t ? rows : cols;
-  return count_for(orows, ocols, t ? transposed_granularity(g) : g);
-}
-
-fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx, fp8q_granularity g,
-                          unsigned flags, uint8_t* codes, int64_t ldc, float* scales,
-                          struct ihipStream_t* stream) {
-  if (!x || !codes || !scales) return FP8Q_ERR_INVAL;
-  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~(FP8Q_OUT_TRANSPOSED | FP8Q_POW2_SCALE)))
-    return FP8Q_ERR_INVAL;
-  const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
-  if (ldx < cols || ldc < (t ? rows : cols)) return FP8Q_ERR_INVAL;
-  const bool splits_cols = g == FP8Q_BLOCK_1x128 || g == FP8Q_BLOCK_128x128;
-  const bool splits_rows = g == FP8Q_BLOCK_128x1 || g == FP8Q_BLOCK_128x128;
-  if (cols % 16 || (t && rows % 16)) return FP8Q_ERR_UNSUPPORTED;
-  if ((splits_cols && cols % 128) || (splits_rows && rows % 128)) return FP8Q_ERR_UNSUPPORTED;
-  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
-  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || ldx % 8 || ldc % 16)
-    return FP8Q_ERR_ALIGN;
-  fp8q::QuantArgs a;
-  a.x = static_cast<const uint16_t*>(x);
-  a.rows = rows;
-  a.cols = cols;
-  a.ldx = ldx;
-  a.codes = codes;
-  a.ldc = ldc;
-  a.scales = scales;
-  a.pow2 = (flags & FP8Q_POW2_SCALE) != 0;
-  const int64_t n = fp8q_scales_count(rows, cols, g, flags);
-  return from_hip(fp8q::launch_quantize(a, g, t, n, reinterpret_cast<hipStream_t>(stream)));
-}
-
-fp8q_status fp8q_quantize_dual(const void* x, int64_t rows, int64_t cols, int64_t ldx, uint8_t* codes_r,
-                               int64_t ldc_r, float* scales_r, uint8_t* codes_t, int64_t ldc_t, float* scales_t,
-                               struct ihipStream_t* stream) {
-  if (!x || !codes_r || !scales_r || !codes_t || !scales_t) return FP8Q_ERR_INVAL;
-  if (rows <= 0 || cols <= 0 || ldx < cols || ldc_r < cols || ldc_t < rows) return FP8Q_ERR_INVAL;
-  if (rows % 128 || cols % 128) return FP8Q_ERR_UNSUPPORTED;
-  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
-  if (!aligned(x, 16) || !aligned(codes_r, 16) || !aligned(codes_t, 16) || !aligned(scales_r, 4) ||
-      !aligned(scales_t, 4) || ldx % 8 || ldc_r % 16 || ldc_t % 16)
-    return FP8Q_ERR_ALIGN;
-  fp8q::DualArgs d;
-  d.a.x = static_cast<const uint16_t*>(x);
-  d.a.rows = rows;
-  d.a.cols = cols;
-  d.a.ldx = ldx;
-  d.a.codes = codes_r;
-  d.a.ldc = ldc_r;
-  d.a.scales = scales_r;
-  d.a.pow2 = 0;
-  d.codes_t = codes_t;
-  d.ldc_t = ldc_t;
-  d.scales_t = scales_t;
-  return from_hip(fp8q::launch_quantize_dual(d, reinterpret_cast<hipStream_t>(stream)));
-}
-
-fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
-                      const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
-                      void* C, int64_t ldc, struct ihipStream_t* stream) {
+// fp8q_gemm with operand formats (FP8Q_A_E5M2 / FP8Q_B_E5M2 bits, only for
+// the two blockwise pairs).
+fp8q_status gemm_checked(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                         const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                         unsigned formats, void* C, int64_t ldc, struct ihipStream_t* stream) {
   if (!A || !sA || !B || !sB || !C) return FP8Q_ERR_INVAL;
+  if (formats & ~(unsigned)(FP8Q_A_E5M2 | FP8Q_B_E5M2)) return FP8Q_ERR_INVAL;
   if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
   if (lda < K || ldb < K || ldc < N) return FP8Q_ERR_INVAL;
   int pair;
@@ -138,6 +78,7 @@ fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, in
     pair = fp8q::kPairBlockK;
   else
     return FP8Q_ERR_UNSUPPORTED;
+  if (formats && pair != fp8q::kPairBlock && pair != fp8q::kPairBlockK) return FP8Q_ERR_UNSUPPORTED;
   if (K % 128 || (gB == FP8Q_BLOCK_128x128 && N % 128)) return FP8Q_ERR_UNSUPPORTED;
   if (((M + 127) / 128) * ((N + 127) / 128) > 0x7fffffff) return FP8Q_ERR_UNSUPPORTED;
   if (!aligned(A, 16) || !aligned(B, 16) || lda % 16 || ldb % 16 || !aligned(C, 8) || ldc % 4 ||
@@ -164,7 +105,87 @@ fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, in
   g.Cs = nullptr;
   g.ldq = 0;
   g.cs_ld = 0;
-  return from_hip(fp8q::launch_gemm(g, pair, reinterpret_cast<hipStream_t>(stream)));
+  return from_hip(fp8q::launch_gemm(g, pair, (int)formats, reinterpret_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g, unsigned flags) {
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~kQuantFlags))
+    return -1;
+  const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
+  const int64_t orows = t ? cols : rows, ocols = t ? rows : cols;
+  return count_for(orows, ocols, t ? transposed_granularity(g) : g);
+}
+
+fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx, fp8q_granularity g,
+                          unsigned flags, uint8_t* codes, int64_t ldc, float* scales,
+                          struct ihipStream_t* stream) {
+  if (!x || !codes || !scales) return FP8Q_ERR_INVAL;
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~kQuantFlags)) return FP8Q_ERR_INVAL;
+  const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
+  if (ldx < cols || ldc < (t ? rows : cols)) return FP8Q_ERR_INVAL;
+  const bool splits_cols = g == FP8Q_BLOCK_1x128 || g == FP8Q_BLOCK_128x128;
+  const bool splits_rows = g == FP8Q_BLOCK_128x1 || g == FP8Q_BLOCK_128x128;
+  if (cols % 16 || (t && rows % 16)) return FP8Q_ERR_UNSUPPORTED;
+  if ((splits_cols && cols % 128) || (splits_rows && rows % 128)) return FP8Q_ERR_UNSUPPORTED;
+  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || ldx % 8 || ldc % 16)
+    return FP8Q_ERR_ALIGN;
+  fp8q::QuantArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.rows = rows;
+  a.cols = cols;
+  a.ldx = ldx;
+  a.codes = codes;
+  a.ldc = ldc;
+  a.scales = scales;
+  a.pow2 = (flags & FP8Q_POW2_SCALE) != 0;
+  a.e5m2 = (flags & FP8Q_E5M2) != 0;
+  const int64_t n = fp8q_scales_count(rows, cols, g, flags);
+  return from_hip(fp8q::launch_quantize(a, g, t, n, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_quantize_dual(const void* x, int64_t rows, int64_t cols, int64_t ldx, unsigned flags,
+                               uint8_t* codes_r, int64_t ldc_r, float* scales_r, uint8_t* codes_t, int64_t ldc_t,
+                               float* scales_t, struct ihipStream_t* stream) {
+  if (!x || !codes_r || !scales_r || !codes_t || !scales_t) return FP8Q_ERR_INVAL;
+  if (flags & ~(unsigned)(FP8Q_POW2_SCALE | FP8Q_E5M2)) return FP8Q_ERR_INVAL;
+  if (rows <= 0 || cols <= 0 || ldx < cols || ldc_r < cols || ldc_t < rows) return FP8Q_ERR_INVAL;
+  if (rows % 128 || cols % 128) return FP8Q_ERR_UNSUPPORTED;
+  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
+  if (!aligned(x, 16) || !aligned(codes_r, 16) || !aligned(codes_t, 16) || !aligned(scales_r, 4) ||
+      !aligned(scales_t, 4) || ldx % 8 || ldc_r % 16 || ldc_t % 16)
+    return FP8Q_ERR_ALIGN;
+  fp8q::DualArgs d;
+  d.a.x = static_cast<const uint16_t*>(x);
+  d.a.rows = rows;
+  d.a.cols = cols;
+  d.a.ldx = ldx;
+  d.a.codes = codes_r;
+  d.a.ldc = ldc_r;
+  d.a.scales = scales_r;
+  d.a.pow2 = (flags & FP8Q_POW2_SCALE) != 0;
+  d.a.e5m2 = (flags & FP8Q_E5M2) != 0;
+  d.codes_t = codes_t;
+  d.ldc_t = ldc_t;
+  d.scales_t = scales_t;
+  return from_hip(fp8q::launch_quantize_dual(d, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                      const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                      void* C, int64_t ldc, struct ihipStream_t* stream) {
+  return gemm_checked(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, 0u, C, ldc, stream);
+}
+
+fp8q_status fp8q_gemm_formats(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda,
+                              const uint8_t* B, const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M,
+                              int64_t N, int64_t K, unsigned formats, void* C, int64_t ldc,
+                              struct ihipStream_t* stream) {
+  return gemm_checked(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, formats, C, ldc, stream);
 }
 
 fp8q_status fp8q_gemm_pow2(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
@@ -200,7 +221,7 @@ fp8q_status fp8q_gemm_pow2(const uint8_t* A, const float* sA, fp8q_granularity g
   g.Cs = nullptr;
   g.ldq = 0;
   g.cs_ld = 0;
-  return from_hip(fp8q::launch_gemm(g, fp8q::kPairBlockE8, reinterpret_cast<hipStream_t>(stream)));
+  return from_hip(fp8q::launch_gemm(g, fp8q::kPairBlockE8, 0, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_gemm_quantized(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda,
@@ -292,7 +313,14 @@ fp8q_status fp8q_calibrate_clip(const float* adv, const float* w_tis, const floa
 fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, struct ihipStream_t* stream) {
   if (!x || !codes || n <= 0 || !(scale > 0.0f)) return FP8Q_ERR_INVAL;
   if (!aligned(x, 4)) return FP8Q_ERR_ALIGN;
-  return from_hip(fp8q::launch_cast_f32(x, n, scale, codes, reinterpret_cast<hipStream_t>(stream)));
+  return from_hip(fp8q::launch_cast_f32(x, n, scale, false, codes, reinterpret_cast<hipStream_t>(stream)));
+}
+
+fp8q_status fp8q_cast_f32_e5m2(const float* x, int64_t n, float scale, uint8_t* codes,
+                               struct ihipStream_t* stream) {
+  if (!x || !codes || n <= 0 || !(scale > 0.0f)) return FP8Q_ERR_INVAL;
+  if (!aligned(x, 4)) return FP8Q_ERR_ALIGN;
+  return from_hip(fp8q::launch_cast_f32(x, n, scale, true, codes, reinterpret_cast<hipStream_t>(stream)));
 }
 
 const char* fp8q_status_string(fp8q_status s) {

@@ -39,9 +39,14 @@ constexpr int kGroupM = 8;  // tile rows per group of the raster
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// Operand formats of a GEMM: bit 0 set when A's codes are E5M2, bit 1 when
+// B's are (else E4M3).  B's tile is the instruction's first operand and A's
+// its second, so B's format goes to the first format field (cbsz) and A's to
+// the second (blgp); 0 selects E4M3 (fp8), 1 E5M2 (bf8).
+template <int FMT>
 __device__ __forceinline__ v4f mfma_16x16x128(const v8i& a, const v8i& b, const v4f& c) {
-  // Scale operands 0 select the unscaled E4M3 x E4M3 instruction.
-  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+  // Scale operands 0 select the unscaled instruction.
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, (FMT >> 1) & 1, FMT & 1, 0, 0, 0, 0);
 }
 
 // The same with power-of-two block scales applied inside the instruction:
@@ -319,7 +324,7 @@ __device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t
 // each owning WM x WN as (WM/16) x (WN/16) MFMA tiles of 16 x 16.  QOUT: the
 // tile leaves as E4M3 codes and 1x128 scales of its bf16 values (see
 // store_quantized) instead of bf16.
-template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT>
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
   constexpr int kWavesN = BN / WN;
   constexpr int kWaves = (BM / WM) * kWavesN;
@@ -641,7 +646,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
             if constexpr (j == 0) se_a = e8m0_of(sa_e[i]);
             acc[i][j] = mfma_16x16x128_e8(bf[j], af, acc[i][j], se_b, se_a);
           } else {
-            acc[i][j] = mfma_16x16x128(bf[j], af, acc[i][j]);
+            acc[i][j] = mfma_16x16x128<FMT>(bf[j], af, acc[i][j]);
           }
           after_mfma(ic, jc);
         });
@@ -677,7 +682,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
       static_for<TJ>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
         wait_b(jc);
-        p[j] = mfma_16x16x128(bf[j], af, zero);
+        p[j] = mfma_16x16x128<FMT>(bf[j], af, zero);
         sched_fence();
       });
       mid_barrier();
@@ -694,7 +699,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
           lds_wait<kAfter + (i == 0 ? kScaleReads : 0)>(af_next);
           static_for<TJ>([&](auto jc) {
             constexpr int j = decltype(jc)::value;
-            p_next[j] = mfma_16x16x128(bf[j], af_next, zero);
+            p_next[j] = mfma_16x16x128<FMT>(bf[j], af_next, zero);
             after_mfma(ic, jc);
           });
         } else {
@@ -820,12 +825,12 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   }
 }
 
-template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT>
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
 hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
   constexpr int threads = (BM / WM) * (BN / WN) * 64;
-  gemm_kernel<PAIR, BM, BN, WM, WN, QOUT><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
+  gemm_kernel<PAIR, BM, BN, WM, WN, QOUT, FMT><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
   return hipGetLastError();
 }
 
@@ -834,24 +839,24 @@ hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
 // once; else 64 x 64 tiles (4 waves of 32 x 32), for skinny problems such as
 // a decode step, whose time goes into streaming the weights.  Quantized
 // output needs whole 128-column units in a tile: 256 or 128 tiles only.
-template <int PAIR, bool QOUT>
+template <int PAIR, bool QOUT, int FMT>
 hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
   const int64_t mid_tiles = ((g.M + 127) / 128) * ((g.N + 127) / 128);
   if constexpr (PAIR != kPairBlockK) {
-    if (big_tiles >= 512) return launch_tiles<PAIR, 256, 256, 128, 64, QOUT>(g, s);
+    if (big_tiles >= 512) return launch_tiles<PAIR, 256, 256, 128, 64, QOUT, FMT>(g, s);
   }
   if constexpr (QOUT) {
-    return launch_tiles<PAIR, 128, 128, 64, 64, QOUT>(g, s);
+    return launch_tiles<PAIR, 128, 128, 64, 64, QOUT, FMT>(g, s);
   } else {
-    if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64, QOUT>(g, s);
-    return launch_tiles<PAIR, 64, 64, 32, 32, QOUT>(g, s);
+    if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64, QOUT, FMT>(g, s);
+    return launch_tiles<PAIR, 64, 64, 32, 32, QOUT, FMT>(g, s);
   }
 }
 
 // The kernels address operands with 32-bit offsets: split the problem into
 // sub-GEMMs whose A and B row ranges each span less than 4 GiB.
-template <int PAIR, bool QOUT>
+template <int PAIR, bool QOUT, int FMT>
 hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
   // 32-bit offsets: each sub-problem's A rows, B rows and C rows span
   // < 2 GiB, and row / column indices stay below 2^31 / 4
@@ -890,7 +895,7 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
       sub.sB = g.sB + db;
       sub.sa_count = g.sa_count - da;
       sub.sb_count = g.sb_count - db;
-      hipError_t e = launch_pair<PAIR, QOUT>(sub, s);
+      hipError_t e = launch_pair<PAIR, QOUT, FMT>(sub, s);
       if (e != hipSuccess) return e;
     }
   }
@@ -900,7 +905,12 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
 // Explicit instantiations: the host pass otherwise emits launch stubs only
 // for the first instantiated pair.
 #define FP8Q_GEMM_KERNEL(PAIR, BM, BN, WM, WN) \
-  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN, false>(GemmArgs);
+  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN, false, 0>(GemmArgs);
+// the backward pairs with E5M2 operands (formats 1, 2, 3)
+#define FP8Q_GEMM_KERNEL_FMT(PAIR, BM, BN, WM, WN)                               \
+  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN, false, 1>(GemmArgs); \
+  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN, false, 2>(GemmArgs); \
+  template __global__ void gemm_kernel<PAIR, BM, BN, WM, WN, false, 3>(GemmArgs);
 FP8Q_GEMM_KERNEL(kPairTensor, 256, 256, 128, 64)
 FP8Q_GEMM_KERNEL(kPairTensor, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairRow, 256, 256, 128, 64)
@@ -915,28 +925,46 @@ FP8Q_GEMM_KERNEL(kPairBlockK, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairBlockE8, 256, 256, 128, 64)
 FP8Q_GEMM_KERNEL(kPairBlockE8, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairBlockE8, 64, 64, 32, 32)
+FP8Q_GEMM_KERNEL_FMT(kPairBlock, 256, 256, 128, 64)
+FP8Q_GEMM_KERNEL_FMT(kPairBlock, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL_FMT(kPairBlock, 64, 64, 32, 32)
+FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 64, 64, 32, 32)
 #undef FP8Q_GEMM_KERNEL
-template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true>(GemmArgs);
-template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true>(GemmArgs);
+#undef FP8Q_GEMM_KERNEL_FMT
+template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true, 0>(GemmArgs);
+template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true, 0>(GemmArgs);
 
 }  // namespace gemm_detail
 
 using namespace gemm_detail;
 
-hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s) {
+template <int PAIR>
+hipError_t launch_formats(const GemmArgs& g, int formats, hipStream_t s) {
+  switch (formats) {
+    case 0: return launch_split<PAIR, false, 0>(g, s);
+    case 1: return launch_split<PAIR, false, 1>(g, s);
+    case 2: return launch_split<PAIR, false, 2>(g, s);
+    case 3: return launch_split<PAIR, false, 3>(g, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm(const GemmArgs& g, int pair, int formats, hipStream_t s) {
+  if (formats != 0 && pair != kPairBlock && pair != kPairBlockK) return hipErrorInvalidValue;
   switch (pair) {
-    case kPairTensor: return launch_split<kPairTensor, false>(g, s);
-    case kPairRow: return launch_split<kPairRow, false>(g, s);
-    case kPairBlock: return launch_split<kPairBlock, false>(g, s);
-    case kPairBlockK: return launch_split<kPairBlockK, false>(g, s);
-    case kPairBlockE8: return launch_split<kPairBlockE8, false>(g, s);
+    case kPairTensor: return launch_split<kPairTensor, false, 0>(g, s);
+    case kPairRow: return launch_split<kPairRow, false, 0>(g, s);
+    case kPairBlock: return launch_formats<kPairBlock>(g, formats, s);
+    case kPairBlockK: return launch_formats<kPairBlockK>(g, formats, s);
+    case kPairBlockE8: return launch_split<kPairBlockE8, false, 0>(g, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s) {
   if (pair != kPairBlock || g.N % 128) return hipErrorInvalidValue;
-  return launch_split<kPairBlock, true>(g, s);
+  return launch_split<kPairBlock, true, 0>(g, s);
 }
 
 }  // namespace fp8q

@@ -15,12 +15,13 @@ struct QuantArgs {
   int64_t ldc;
   float* scales;
   int pow2;           // power-of-two scales (FP8Q_POW2_SCALE)
+  int e5m2;           // E5M2 codes, F_max = 57344 (FP8Q_E5M2)
 };
 
 // granularity: the fp8q_granularity value; nscales: entries of `scales`.
 hipError_t launch_quantize(const QuantArgs& a, int granularity, bool transposed, int64_t nscales,
                            hipStream_t s);
-hipError_t launch_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, hipStream_t s);
+hipError_t launch_cast_f32(const float* x, int64_t n, float scale, bool e5m2, uint8_t* codes, hipStream_t s);
 
 // Both backward-pass layouts from one read: `a` carries x and the 1x128
 // output (codes [rows][ldc], scales [cols/128][rows]); codes_t / scales_t
@@ -36,8 +37,8 @@ struct DualArgs {
 hipError_t launch_quantize_dual(const DualArgs& d, hipStream_t s);
 
 struct GemmArgs {
-  const uint8_t* A;  // E4M3 [M][lda]
-  const uint8_t* B;  // E4M3 [N][ldb]
+  const uint8_t* A;  // FP8 codes [M][lda] (E4M3, or E5M2 by the formats)
+  const uint8_t* B;  // FP8 codes [N][ldb]
   const float* sA;
   const float* sB;
   uint16_t* C;       // bf16 [M][ldc]
@@ -60,7 +61,9 @@ struct GemmArgs {
 // the matrix instruction)
 enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3, kPairBlockE8 = 4 };
 
-hipError_t launch_gemm(const GemmArgs& g, int pair, hipStream_t s);
+// formats: bit 0 = A's codes are E5M2, bit 1 = B's (kPairBlock and
+// kPairBlockK only; 0 for E4M3 x E4M3).
+hipError_t launch_gemm(const GemmArgs& g, int pair, int formats, hipStream_t s);
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s);
 
 // Calibrated Clipping: per-token float32 arrays of n tokens, the grids

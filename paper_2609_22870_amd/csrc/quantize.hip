@@ -104,12 +104,13 @@ __device__ __noinline__ float slow_quotient(float x, float s, float r) {
 // all of them.
 enum UnitMap { kUnitRow, kUnitCol, kUnitOne };
 
-// Codes of a thread's 8 x 8 patch, two E4M3 bytes per conversion: byte j of
+// Codes of a thread's 8 x 8 patch (E4M3, or E5M2 when E5), two bytes per
+// conversion: byte j of
 // packed[i][j / 4] is element (i, j), with the unit scales su (S) and ru
 // (1/S) indexed by row, by column, or [0].  The reciprocal-based quotient
 // holds for S >= 2^-90 (see quotient()); waves whose units all satisfy it
 // take the branch-free path.
-template <int MAP>
+template <int MAP, bool E5>
 __device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8], const float (&ru)[8],
                                              uint32_t (&packed)[8][2]) {
   bool fast = true;
@@ -127,8 +128,8 @@ __device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8]
           const int u = MAP == kUnitRow ? i : (MAP == kUnitCol ? j : 0);
           q[jj] = qf(t.v[i][j], su[u], ru[u]);
         }
-        uint32_t w = e4m3_pack2<false>(q[0], q[1], 0u);
-        packed[i][h] = e4m3_pack2<true>(q[2], q[3], w);
+        uint32_t w = fp8_pack2<E5, false>(q[0], q[1], 0u);
+        packed[i][h] = fp8_pack2<E5, true>(q[2], q[3], w);
       }
     }
   };
@@ -142,10 +143,11 @@ __device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8]
 // 16 lanes of its DPP row: lane cc of the row group holds the amax of row
 // cc % 8, computes that unit's S and 1/S (two IEEE divisions), and the
 // group exchanges them by lane shuffles.
+template <bool E5>
 __device__ __forceinline__ void share_row_units(float amax, bool pow2, UnitScale& mine, float (&su)[8],
                                                 float (&ru)[8]) {
   const int lane = threadIdx.x & 63;
-  mine = unit_scale(amax, pow2);
+  mine = unit_scale_fmt<E5>(amax, pow2);
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     su[i] = __shfl(mine.s, (lane & 48) | i, 64);
@@ -157,10 +159,11 @@ __device__ __forceinline__ void share_row_units(float amax, bool pow2, UnitScale
 // (rg < 8, cc) holds the amax of column 8 cc + rg, computes its S and 1/S,
 // and the block exchanges them through LDS (the upper half of lds_red, after
 // every read of its lower half).
+template <bool E5>
 __device__ __forceinline__ void share_col_units(float amax, bool pow2, float* lds_red, UnitScale& mine,
                                                 float (&su)[8], float (&ru)[8]) {
   const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  mine = unit_scale(amax, pow2);
+  mine = unit_scale_fmt<E5>(amax, pow2);
   float2* lds_su = reinterpret_cast<float2*>(lds_red + 2 * kTile);
   __syncthreads();
   if (rg < 8) lds_su[cc * 8 + rg] = make_float2(mine.s, mine.r);
@@ -234,7 +237,7 @@ __device__ __forceinline__ void store_patch_transposed(const uint32_t (&packed)[
   }
 }
 
-template <int K, bool TRANS>
+template <int K, bool TRANS, bool E5>
 __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   __shared__ float lds_red[4 * kTile];
   __shared__ uint64_t lds_t[TRANS ? kTile * kTile / 8 : 1];
@@ -276,7 +279,7 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       const int64_t r = row0 + (cc & 7);
       amax = r < a.rows ? a.scales[r] : 0.0f;
     }
-    share_row_units(amax, a.pow2 != 0, mine, su, ru);
+    share_row_units<E5>(amax, a.pow2 != 0, mine, su, ru);
   } else if (by_col) {
     float amax;
     if (K == kBlock128x1) {
@@ -289,9 +292,9 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       const int64_t cj = c0 + cc * 8 + (rg & 7);
       amax = cj < a.cols ? a.scales[cj] : 0.0f;
     }
-    share_col_units(amax, a.pow2 != 0, lds_red, mine, su, ru);
+    share_col_units<E5>(amax, a.pow2 != 0, lds_red, mine, su, ru);
   } else {
-    mine = unit_scale(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0], a.pow2 != 0);
+    mine = unit_scale_fmt<E5>(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0], a.pow2 != 0);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       su[i] = mine.s;
@@ -300,7 +303,7 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   }
 
   uint32_t packed[8][2];
-  encode_patch<by_row ? kUnitRow : (by_col ? kUnitCol : kUnitOne)>(t, su, ru, packed);
+  encode_patch<by_row ? kUnitRow : (by_col ? kUnitCol : kUnitOne), E5>(t, su, ru, packed);
 
   if (!TRANS)
     store_patch(packed, a.codes, a.ldc, a.rows, a.cols, row0, c);
@@ -332,6 +335,7 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
 // columns), with codes stored transposed, codes_t[c][r], and scales at
 // (r / 128) * cols + c.  Each half is the single-layout kernel's work, so
 // each result is byte-identical to it.
+template <bool E5>
 __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
   __shared__ float lds_red[4 * kTile];
   __shared__ uint64_t lds_t[kTile * kTile / 8];
@@ -347,8 +351,8 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
   UnitScale mine;
   float su[8], ru[8];
 
-  share_row_units(block_row_amax(t), a.pow2 != 0, mine, su, ru);
-  encode_patch<kUnitRow>(t, su, ru, packed);
+  share_row_units<E5>(block_row_amax(t), a.pow2 != 0, mine, su, ru);
+  encode_patch<kUnitRow, E5>(t, su, ru, packed);
   store_patch(packed, a.codes, a.ldc, a.rows, a.cols, row0, c);
   {
     const int64_t r = row0 + cc;
@@ -360,8 +364,8 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
   float amax = m[0];
 #pragma unroll
   for (int j = 1; j < 8; ++j) amax = (rg & 7) == j ? m[j] : amax;
-  share_col_units(amax, a.pow2 != 0, lds_red, mine, su, ru);
-  encode_patch<kUnitCol>(t, su, ru, packed);
+  share_col_units<E5>(amax, a.pow2 != 0, lds_red, mine, su, ru);
+  encode_patch<kUnitCol, E5>(t, su, ru, packed);
   store_patch_transposed(packed, lds_t, d.codes_t, d.ldc_t, a.rows, a.cols, r0, c0);
   const int64_t cj = c0 + cc * 8 + rg;
   if (rg < 8 && cj < a.cols) d.scales_t[tr * a.cols + cj] = mine.s;
@@ -430,6 +434,7 @@ __device__ __forceinline__ void load_row_chunk(const QuantArgs& a, const uint16_
   }
 }
 
+template <bool E5>
 __global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) {
   const int lane = threadIdx.x & 63;
   const bool one_chunk = a.cols <= kRowChunk;
@@ -443,7 +448,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) 
 #pragma unroll
       for (int q = 0; q < 8; ++q) m = fmaxf(m, row_partial_max(t, q));
     }
-    const UnitScale u = unit_scale(wave_max(m), a.pow2 != 0);
+    const UnitScale u = unit_scale_fmt<E5>(wave_max(m), a.pow2 != 0);
     float su[8], ru[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -453,7 +458,7 @@ __global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) 
     for (int64_t c0 = 0; c0 < a.cols; c0 += kRowChunk) {
       if (!one_chunk) load_row_chunk(a, xr, c0, t);
       uint32_t packed[8][2];
-      encode_patch<kUnitOne>(t, su, ru, packed);
+      encode_patch<kUnitOne, E5>(t, su, ru, packed);
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
         const int64_t c = c0 + q * 512 + lane * 8;
@@ -494,28 +499,30 @@ __global__ void fill_zero_kernel(float* p, int64_t n) {
     p[i] = 0.0f;
 }
 
+template <bool E5>
 __global__ void amax_to_scale_kernel(float* p, int64_t n, int pow2) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = unit_scale(p[i], pow2 != 0).s;
+    p[i] = unit_scale_fmt<E5>(p[i], pow2 != 0).s;
 }
 
+template <bool E5>
 __global__ void cast_f32_kernel(const float* x, int64_t n, float scale, uint8_t* codes) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
     const float q = x[i] / scale;  // IEEE division: any fp32 x and scale
-    codes[i] = (uint8_t)(e4m3_pack2<false>(q, q, 0u) & 0xffu);
+    codes[i] = (uint8_t)(fp8_pack2<E5, false>(q, q, 0u) & 0xffu);
   }
 }
 
-template <int K, bool TRANS>
+template <int K, bool TRANS, bool E5>
 hipError_t launch_tile(const QuantArgs& a, hipStream_t s) {
   constexpr bool kWide = !TRANS && (K == kBlock1x128 || K == kPreRow || K == kPreTensor);
   constexpr int64_t tr = kWide ? kWideRows : kTile, tc = kWide ? kWideCols : kTile;
   const dim3 grid((unsigned)((a.cols + tc - 1) / tc), (unsigned)((a.rows + tr - 1) / tr));
-  quant_tile_kernel<K, TRANS><<<grid, kThreads, 0, s>>>(a);
+  quant_tile_kernel<K, TRANS, E5><<<grid, kThreads, 0, s>>>(a);
   return hipGetLastError();
 }
 
-template <int K>
+template <int K, bool E5>
 hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipStream_t s) {
   const unsigned fill_blocks = (unsigned)((nscales + 255) / 256 < 4096 ? (nscales + 255) / 256 : 4096);
   fill_zero_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales);
@@ -529,10 +536,29 @@ hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipS
     amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  e = trans ? launch_tile<K, true>(a, s) : launch_tile<K, false>(a, s);
+  e = trans ? launch_tile<K, true, E5>(a, s) : launch_tile<K, false, E5>(a, s);
   if (e != hipSuccess) return e;
-  amax_to_scale_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales, a.pow2);
+  amax_to_scale_kernel<E5><<<fill_blocks, 256, 0, s>>>(a.scales, nscales, a.pow2);
   return hipGetLastError();
+}
+
+template <bool E5>
+hipError_t launch_quantize_fmt(const QuantArgs& a, int granularity, bool trans, int64_t nscales, hipStream_t s) {
+  switch (granularity) {
+    case 3: return trans ? launch_tile<kBlock1x128, true, E5>(a, s) : launch_tile<kBlock1x128, false, E5>(a, s);
+    case 4: return trans ? launch_tile<kBlock128x1, true, E5>(a, s) : launch_tile<kBlock128x1, false, E5>(a, s);
+    case 5:
+      return trans ? launch_tile<kBlock128x128, true, E5>(a, s) : launch_tile<kBlock128x128, false, E5>(a, s);
+    case 0: return launch_two_pass<kPreTensor, E5>(a, trans, nscales, s);
+    case 1: {
+      if (trans) return launch_two_pass<kPreRow, E5>(a, trans, nscales, s);
+      const int64_t blocks = (a.rows + kRowWaves - 1) / kRowWaves;
+      quant_row_kernel<E5><<<(unsigned)(blocks < 16384 ? blocks : 16384), kRowWaves * 64, 0, s>>>(a);
+      return hipGetLastError();
+    }
+    case 2: return launch_two_pass<kPreCol, E5>(a, trans, nscales, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace quant_detail
@@ -540,31 +566,26 @@ hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipS
 using namespace quant_detail;
 
 hipError_t launch_quantize(const QuantArgs& a, int granularity, bool trans, int64_t nscales, hipStream_t s) {
-  switch (granularity) {
-    case 3: return trans ? launch_tile<kBlock1x128, true>(a, s) : launch_tile<kBlock1x128, false>(a, s);
-    case 4: return trans ? launch_tile<kBlock128x1, true>(a, s) : launch_tile<kBlock128x1, false>(a, s);
-    case 5: return trans ? launch_tile<kBlock128x128, true>(a, s) : launch_tile<kBlock128x128, false>(a, s);
-    case 0: return launch_two_pass<kPreTensor>(a, trans, nscales, s);
-    case 1: {
-      if (trans) return launch_two_pass<kPreRow>(a, trans, nscales, s);
-      const int64_t blocks = (a.rows + kRowWaves - 1) / kRowWaves;
-      quant_row_kernel<<<(unsigned)(blocks < 16384 ? blocks : 16384), kRowWaves * 64, 0, s>>>(a);
-      return hipGetLastError();
-    }
-    case 2: return launch_two_pass<kPreCol>(a, trans, nscales, s);
-    default: return hipErrorInvalidValue;
-  }
+  return a.e5m2 ? launch_quantize_fmt<true>(a, granularity, trans, nscales, s)
+                : launch_quantize_fmt<false>(a, granularity, trans, nscales, s);
 }
 
 hipError_t launch_quantize_dual(const DualArgs& d, hipStream_t s) {
   const dim3 grid((unsigned)((d.a.cols + kTile - 1) / kTile), (unsigned)((d.a.rows + kTile - 1) / kTile));
-  quant_dual_kernel<<<grid, kThreads, 0, s>>>(d);
+  if (d.a.e5m2)
+    quant_dual_kernel<true><<<grid, kThreads, 0, s>>>(d);
+  else
+    quant_dual_kernel<false><<<grid, kThreads, 0, s>>>(d);
   return hipGetLastError();
 }
 
-hipError_t launch_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, hipStream_t s) {
+hipError_t launch_cast_f32(const float* x, int64_t n, float scale, bool e5m2, uint8_t* codes, hipStream_t s) {
   const int64_t blocks = (n + 255) / 256;
-  cast_f32_kernel<<<(unsigned)(blocks < 8192 ? blocks : 8192), 256, 0, s>>>(x, n, scale, codes);
+  const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);
+  if (e5m2)
+    cast_f32_kernel<true><<<grid, 256, 0, s>>>(x, n, scale, codes);
+  else
+    cast_f32_kernel<false><<<grid, 256, 0, s>>>(x, n, scale, codes);
   return hipGetLastError();
 }
 

@@ -14,19 +14,19 @@ _ROW_LOCAL = {oracle.BLOCK_1x128: 1, oracle.BLOCK_128x1: 128,
               oracle.BLOCK_128x128: 128, oracle.ROW: 1}
 
 
-def quantize(x_bits, g, transposed=False, threads=THREADS, pow2=False):
+def quantize(x_bits, g, transposed=False, threads=THREADS, pow2=False, e5m2=False):
     """oracle.quantize on a [rows, cols] bf16 bit array, split into row chunks
     when the granularity's units do not cross rows of the chunking."""
     rows, cols = x_bits.shape
     step = _ROW_LOCAL.get(g)
     if step is None or rows <= 1024:
-        return oracle.quantize(x_bits, g, transposed, pow2)
+        return oracle.quantize(x_bits, g, transposed, pow2, e5m2)
     nchunk = min(threads * 4, rows // step)
     bounds = np.linspace(0, rows // step, nchunk + 1).astype(np.int64) * step
     bounds[-1] = rows
     parts = [(int(a), int(b)) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]
     with ThreadPoolExecutor(threads) as ex:
-        res = list(ex.map(lambda ab: oracle.quantize(x_bits[ab[0]:ab[1]], g, transposed, pow2), parts))
+        res = list(ex.map(lambda ab: oracle.quantize(x_bits[ab[0]:ab[1]], g, transposed, pow2, e5m2), parts))
     codes = np.concatenate([c for c, _ in res], axis=1 if transposed else 0)
     if g == oracle.BLOCK_1x128:       # [cols/128][rows], chunks along rows
         scales = np.concatenate([s.reshape(cols // 128, -1) for _, s in res], axis=1).reshape(-1)
@@ -37,18 +37,18 @@ def quantize(x_bits, g, transposed=False, threads=THREADS, pow2=False):
     return codes, scales
 
 
-def gemm_rows(A, sA, gA, B, sB, gB, rows, threads=THREADS):
+def gemm_rows(A, sA, gA, B, sB, gB, rows, threads=THREADS, fmtA=oracle.FMT_E4M3, fmtB=oracle.FMT_E4M3):
     rows = np.asarray(rows, dtype=np.int64)
     parts = np.array_split(rows, max(1, min(threads * 2, rows.size)))
     with ThreadPoolExecutor(threads) as ex:
-        res = list(ex.map(lambda r: oracle.gemm_rows(A, sA, gA, B, sB, gB, r), parts))
+        res = list(ex.map(lambda r: oracle.gemm_rows(A, sA, gA, B, sB, gB, r, fmtA, fmtB), parts))
     return np.concatenate(res, axis=0)
 
 
-def cast_f32(x, scale, threads=THREADS):
+def cast_f32(x, scale, threads=THREADS, e5m2=False):
     parts = np.array_split(x, threads * 4)
     with ThreadPoolExecutor(threads) as ex:
-        res = list(ex.map(lambda p: oracle.cast_f32(p, scale), parts))
+        res = list(ex.map(lambda p: oracle.cast_f32(p, scale, e5m2), parts))
     return np.concatenate(res)
 
 

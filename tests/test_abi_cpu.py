@@ -77,7 +77,7 @@ def test_quantize_rejections(L):
     assert quant(L, rows=0) == -1
     assert quant(L, cols=-5) == -1
     assert quant(L, g=6) == -1
-    assert quant(L, flags=4) == -1                           # unknown flag bit
+    assert quant(L, flags=8) == -1                           # unknown flag bit
     assert quant(L, ldx=128) == -1
     assert quant(L, ldc=128) == -1
     assert quant(L, cols=200, ldx=200, ldc=208) == -2        # cols % 16
@@ -132,13 +132,40 @@ def test_gemm_pow2_rejections(L):
     assert gp(ldc=258) == -3
 
 
-def test_scales_count_pow2_flag(L):
+def test_scales_count_pow2_and_e5m2_flags(L):
     assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 2) == 256 * 3
     assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 3) == 256 * 3
-    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 4) == -1
+    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 4) == 256 * 3    # E5M2
+    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 7) == 256 * 3
+    assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 8) == -1
 
 
-def test_cast_rejections(L):
+def gemm_f(L, formats, **kw):
+    args = dict(A=FAKE, sA=FAKE, gA=3, lda=256, B=FAKE, sB=FAKE, gB=5, ldb=256, M=256, N=256, K=256)
+    args.update(kw)
+    return L.fp8q_gemm_formats(*args.values(), formats, FAKE, 256, None)
+
+
+def test_gemm_formats_rejections(L):
+    assert gemm_f(L, 4) == -1                                # unknown format bit
+    assert gemm_f(L, 1, A=None) == -1
+    assert gemm_f(L, 1, gA=0, gB=0) == -2                    # E5M2 only for the blockwise pairs
+    assert gemm_f(L, 2, gA=1, gB=1) == -2
+    assert gemm_f(L, 3, N=200) == -2
+    assert gemm_f(L, 1, A=FAKE + 4) == -3
+    assert gemm_f(L, 1, gA=3, gB=3, lda=264) == -3
+
+
+@pytest.mark.parametrize("name", ["fp8q_cast_f32", "fp8q_cast_f32_e5m2"])
+def test_cast_rejections(L, name):
+    fn = getattr(L, name)
+    assert fn(None, 10, 1.0, FAKE, None) == -1
+    assert fn(FAKE, 0, 1.0, FAKE, None) == -1
+    assert fn(FAKE, 10, 0.0, FAKE, None) == -1
+    assert fn(FAKE + 1, 10, 1.0, FAKE, None) == -3
+
+
+def test_cast_rejections_e4m3(L):
     assert L.fp8q_cast_f32(None, 10, 1.0, FAKE, None) == -1
     assert L.fp8q_cast_f32(FAKE, 0, 1.0, FAKE, None) == -1
     assert L.fp8q_cast_f32(FAKE, 10, 0.0, FAKE, None) == -1
@@ -154,13 +181,16 @@ def test_no_cpu_fallback_when_library_missing(monkeypatch, tmp_path):
         fp8q.lib()
 
 
-def dual(L, x=FAKE, rows=256, cols=256, ldx=256, cr=FAKE, ldr=256, sr=FAKE,
+def dual(L, x=FAKE, rows=256, cols=256, ldx=256, flags=0, cr=FAKE, ldr=256, sr=FAKE,
          ct=FAKE, ldt=256, st=FAKE):
-    return L.fp8q_quantize_dual(x, rows, cols, ldx, cr, ldr, sr, ct, ldt, st, None)
+    return L.fp8q_quantize_dual(x, rows, cols, ldx, flags, cr, ldr, sr, ct, ldt, st, None)
 
 
 def test_quantize_dual_rejections(L):
     assert dual(L, x=None) == -1
+    assert dual(L, flags=1) == -1                            # transposition is implied, not a flag
+    assert dual(L, flags=8) == -1
+    assert dual(L, flags=6, rows=272, ldt=272) == -2         # pow2 | E5M2 accepted, shape checked
     assert dual(L, cr=None) == -1
     assert dual(L, st=None) == -1
     assert dual(L, rows=0) == -1
