@@ -154,7 +154,10 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
       instruction, with that quantization of X;
     * the E5M2 variant for gradients on the same dY: its dual-layout
       quantization, and the 32B up-projection's data-gradient GEMM dX = dY W
-      (16384 x 25600 -> 5120) with dY's codes in E5M2 against E4M3."""
+      (16384 x 25600 -> 5120) with dY's codes in E5M2 against E4M3;
+    * the grouped GEMM of the fused projections of the step's X (query, key
+      and value: 4096 + 1024 + 1024 outputs; gate and up: 2 x 12288) in one
+      launch, against one fp8q_gemm call per projection."""
     rows, cols = 16384, 25600
     dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
     outs = fp8q.quantize_dual(dy)
@@ -212,6 +215,23 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
     pow2_tflops = 2.0 * M * N * K / (t_pow2 * 1e-6) / 1e12
     del y, xb, sxb, wb, swb
 
+    grouped = {}
+    for kind, widths in (("qkv", (4096, 1024, 1024)), ("gate_up", (12288, 12288))):
+        probs = []
+        for i, n in enumerate(widths):
+            wq_i, sw_i = fp8q.quantize(synth.weights(n, K, seed=synth.seed_for(6, 1, i), device=dev),
+                                       fp8q.BLOCK_128x128)
+            probs.append((xq, sx, wq_i, sw_i))
+        outs = fp8q.gemm_grouped(probs, fp8q.BLOCK_1x128, fp8q.BLOCK_128x128)
+        t_grp = timed(lambda: fp8q.gemm_grouped(probs, fp8q.BLOCK_1x128, fp8q.BLOCK_128x128, outs=outs))
+        t_sep = timed(lambda: [fp8q.gemm(a, sa, fp8q.BLOCK_1x128, b, sb, fp8q.BLOCK_128x128, out=c)
+                               for (a, sa, b, sb), c in zip(probs, outs)])
+        flops = 2.0 * M * K * sum(widths)
+        grouped[kind] = {"widths": list(widths), "us": round(t_grp, 1),
+                         "tflops": round(flops / (t_grp * 1e-6) / 1e12, 1),
+                         "separate_calls_us": round(t_sep, 1)}
+        del probs, outs
+
     rl = {k: v.to(dev) for k, v in synth.rl_batch(**synth.RL_BATCH, seed=5001).items()}
     keys = ("adv", "w_tis", "pi_sampler", "r_bf16", "r_fp8")
     ntok = rl["adv"].numel()
@@ -236,6 +256,7 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
         "dual_quantize_us": round(t_dual5, 1), "dgrad_shape": [rows, cols, k_in],
         "dgrad_e5m2_us": round(t_dg5, 1), "dgrad_e5m2_tflops": round(dg_flops / (t_dg5 * 1e-6) / 1e12, 1),
         "dgrad_e4m3_us": round(t_dg4, 1), "dgrad_e4m3_tflops": round(dg_flops / (t_dg4 * 1e-6) / 1e12, 1)},
+        "gemm_grouped_8b_fused_projections": grouped,
         "calibrated_clipping_grpo_batch": {
         "tokens": ntok, "us": round(t_clip, 1), "gbs": round(clip_gbs, 1),
         "frac_hbm": round(clip_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": round(clip_bytes)}}

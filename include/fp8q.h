@@ -164,6 +164,41 @@ fp8q_status fp8q_gemm(const uint8_t *A, const float *sA, fp8q_granularity gA,
                       int64_t K, void *C, int64_t ldc,
                       struct ihipStream_t *stream);
 
+/* One problem of fp8q_gemm_grouped: the arguments of fp8q_gemm that differ
+ * between the problems (pointers, leading dimensions, M and N). */
+typedef struct fp8q_gemm_problem {
+  const uint8_t *A;   /* codes [M][lda] */
+  const float *sA;
+  int64_t lda;
+  const uint8_t *B;   /* codes [N][ldb] */
+  const float *sB;
+  int64_t ldb;
+  void *C;            /* bf16 [M][ldc] */
+  int64_t ldc;
+  int64_t M, N;
+} fp8q_gemm_problem;
+
+enum { FP8Q_MAX_GROUP = 8 };
+
+/*
+ * Several fp8q_gemm problems in one launch: the grouped GEMM of fused
+ * projections that share their input (the FP8 linear layers of Sec. 5.3,
+ * e.g. the query, key and value projections, or the gate and up
+ * projections of an MLP, each with its own weight and output).  Each
+ * problems[i] (a host array of 1 .. FP8Q_MAX_GROUP entries, read before the
+ * call returns) computes C_i = dequant(A_i) dequant(B_i)^T exactly as
+ * fp8q_gemm(A_i, sA_i, gA, lda_i, B_i, sB_i, gB, ldb_i, M_i, N_i, K, C_i,
+ * ldc_i) would, with every rule of fp8q_gemm per problem; the A_i may be
+ * the same operand.  Supported (gA, gB): (TENSOR, TENSOR), (ROW, ROW) and
+ * (1x128, 128x128) (else FP8Q_ERR_UNSUPPORTED).  Each problem's A, B and C
+ * must each span less than 2 GiB (M lda, N ldb and 2 M ldc bytes; else
+ * FP8Q_ERR_UNSUPPORTED).  The outputs must not overlap each other or any
+ * input.  count outside 1 .. FP8Q_MAX_GROUP is FP8Q_ERR_INVAL.
+ */
+fp8q_status fp8q_gemm_grouped(const fp8q_gemm_problem *problems, int count,
+                              fp8q_granularity gA, fp8q_granularity gB,
+                              int64_t K, struct ihipStream_t *stream);
+
 /* Operand formats of fp8q_gemm_formats: A's codes, B's codes are E5M2. */
 enum { FP8Q_A_E5M2 = 1u, FP8Q_B_E5M2 = 2u };
 

@@ -25,9 +25,20 @@ _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
            -3: "FP8Q_ERR_ALIGN", -4: "FP8Q_ERR_HIP"}
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
-           "fp8q_gemm", "fp8q_gemm_formats", "fp8q_gemm_pow2", "fp8q_gemm_quantized",
+           "fp8q_gemm", "fp8q_gemm_grouped", "fp8q_gemm_formats", "fp8q_gemm_pow2", "fp8q_gemm_quantized",
            "fp8q_calibrate_clip_workspace", "fp8q_calibrate_clip", "fp8q_cast_f32",
            "fp8q_cast_f32_e5m2", "fp8q_status_string")
+
+
+MAX_GROUP = 8
+
+
+class GemmProblem(ctypes.Structure):
+    """fp8q_gemm_problem of include/fp8q.h."""
+    _fields_ = [("A", ctypes.c_void_p), ("sA", ctypes.c_void_p), ("lda", ctypes.c_int64),
+                ("B", ctypes.c_void_p), ("sB", ctypes.c_void_p), ("ldb", ctypes.c_int64),
+                ("C", ctypes.c_void_p), ("ldc", ctypes.c_int64),
+                ("M", ctypes.c_int64), ("N", ctypes.c_int64)]
 
 
 class ClipConfig(ctypes.Structure):
@@ -76,6 +87,8 @@ def lib():
         L.fp8q_gemm.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
                                 p, i64, p]
         L.fp8q_gemm.restype = i32
+        L.fp8q_gemm_grouped.argtypes = [ctypes.POINTER(GemmProblem), i32, i32, i32, i64, p]
+        L.fp8q_gemm_grouped.restype = i32
         L.fp8q_gemm_formats.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64, u32, p, i64, p]
         L.fp8q_gemm_formats.restype = i32
         L.fp8q_gemm_pow2.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64, p, i64, p]
@@ -199,6 +212,29 @@ def gemm(a, sa, ga, b, sb, gb, out=None):
                          out.data_ptr(), _ld(out), _stream(a))
     _check(st, "fp8q_gemm")
     return out
+
+
+def gemm_grouped(problems, ga, gb, outs=None):
+    """Several gemm() problems in one launch (fp8q_gemm_grouped).
+
+    problems: list of (a, sa, b, sb) with one K and the granularities ga,
+    gb for all (the a's may be the same tensor); returns the bf16 outputs
+    (or fills `outs`)."""
+    if not 1 <= len(problems) <= MAX_GROUP:
+        raise ValueError("1 .. %d problems" % MAX_GROUP)
+    K = problems[0][0].shape[1]
+    if outs is None:
+        outs = [torch.empty((a.shape[0], b.shape[0]), dtype=torch.bfloat16, device=a.device)
+                for a, _, b, _ in problems]
+    arr = (GemmProblem * len(problems))()
+    for i, ((a, sa, b, sb), c) in enumerate(zip(problems, outs)):
+        if a.shape[1] != K or b.shape[1] != K:
+            raise ValueError("every problem must have the same K")
+        arr[i] = GemmProblem(a.data_ptr(), sa.data_ptr(), _ld(a), b.data_ptr(), sb.data_ptr(), _ld(b),
+                             c.data_ptr(), _ld(c), a.shape[0], b.shape[0])
+    st = lib().fp8q_gemm_grouped(arr, len(problems), ga, gb, K, _stream(problems[0][0]))
+    _check(st, "fp8q_gemm_grouped")
+    return outs
 
 
 def gemm_formats(a, sa, ga, b, sb, gb, formats, out=None):

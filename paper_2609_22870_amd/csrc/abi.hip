@@ -58,16 +58,15 @@ bool grid_size(double lo, double hi, double step, int& n) {
   return true;
 }
 
-// fp8q_gemm with operand formats (FP8Q_A_E5M2 / FP8Q_B_E5M2 bits, only for
-// the two blockwise pairs).
-fp8q_status gemm_checked(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
-                         const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
-                         unsigned formats, void* C, int64_t ldc, struct ihipStream_t* stream) {
+// The checks of fp8q_gemm (with operand formats: FP8Q_A_E5M2 / FP8Q_B_E5M2
+// bits, only for the two blockwise pairs), then the kernel arguments.
+fp8q_status gemm_args(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                      const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                      unsigned formats, void* C, int64_t ldc, fp8q::GemmArgs& g, int& pair) {
   if (!A || !sA || !B || !sB || !C) return FP8Q_ERR_INVAL;
   if (formats & ~(unsigned)(FP8Q_A_E5M2 | FP8Q_B_E5M2)) return FP8Q_ERR_INVAL;
   if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
   if (lda < K || ldb < K || ldc < N) return FP8Q_ERR_INVAL;
-  int pair;
   if (gA == FP8Q_TENSOR && gB == FP8Q_TENSOR)
     pair = fp8q::kPairTensor;
   else if (gA == FP8Q_ROW && gB == FP8Q_ROW)
@@ -84,7 +83,6 @@ fp8q_status gemm_checked(const uint8_t* A, const float* sA, fp8q_granularity gA,
   if (!aligned(A, 16) || !aligned(B, 16) || lda % 16 || ldb % 16 || !aligned(C, 8) || ldc % 4 ||
       !aligned(sA, 4) || !aligned(sB, 4))
     return FP8Q_ERR_ALIGN;
-  fp8q::GemmArgs g;
   g.A = A;
   g.B = B;
   g.sA = sA;
@@ -105,6 +103,16 @@ fp8q_status gemm_checked(const uint8_t* A, const float* sA, fp8q_granularity gA,
   g.Cs = nullptr;
   g.ldq = 0;
   g.cs_ld = 0;
+  return FP8Q_OK;
+}
+
+fp8q_status gemm_checked(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                         const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                         unsigned formats, void* C, int64_t ldc, struct ihipStream_t* stream) {
+  fp8q::GemmArgs g;
+  int pair = 0;
+  const fp8q_status st = gemm_args(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, formats, C, ldc, g, pair);
+  if (st != FP8Q_OK) return st;
   return from_hip(fp8q::launch_gemm(g, pair, (int)formats, reinterpret_cast<hipStream_t>(stream)));
 }
 
@@ -186,6 +194,26 @@ fp8q_status fp8q_gemm_formats(const uint8_t* A, const float* sA, fp8q_granularit
                               int64_t N, int64_t K, unsigned formats, void* C, int64_t ldc,
                               struct ihipStream_t* stream) {
   return gemm_checked(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, formats, C, ldc, stream);
+}
+
+fp8q_status fp8q_gemm_grouped(const fp8q_gemm_problem* problems, int count, fp8q_granularity gA,
+                              fp8q_granularity gB, int64_t K, struct ihipStream_t* stream) {
+  if (!problems || count < 1 || count > FP8Q_MAX_GROUP) return FP8Q_ERR_INVAL;
+  static_assert(FP8Q_MAX_GROUP == fp8q::kMaxGroup, "group limits agree");
+  fp8q::GemmGroup gs;
+  int pair = 0;
+  const int64_t lim = (int64_t)1 << 31;
+  for (int i = 0; i < count; ++i) {
+    const fp8q_gemm_problem& p = problems[i];
+    const fp8q_status st =
+        gemm_args(p.A, p.sA, gA, p.lda, p.B, p.sB, gB, p.ldb, p.M, p.N, K, 0u, p.C, p.ldc, gs.prob[i], pair);
+    if (st != FP8Q_OK) return st;
+    if (pair == fp8q::kPairBlockK) return FP8Q_ERR_UNSUPPORTED;
+    // the kernel's 32-bit operand offsets (fp8q_gemm splits such a problem)
+    if (p.M * p.lda >= lim || p.N * p.ldb >= lim || p.M * 2 * p.ldc >= lim) return FP8Q_ERR_UNSUPPORTED;
+  }
+  gs.count = count;
+  return from_hip(fp8q::launch_gemm_grouped(gs, pair, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_gemm_pow2(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,

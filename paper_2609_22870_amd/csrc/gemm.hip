@@ -251,12 +251,15 @@ __device__ __forceinline__ void order_after(v8i& next, v4f (&done)[TJ]) {
 // each XCD is given a contiguous range of the raster (sharing its L2), and
 // the raster walks kGroupM tile rows at a time so that consecutive tiles
 // reuse A rows and B rows.
-template <int BM, int BN>
-__device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int b, int& tm, int& tn) {
-  const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
-  const int total = tiles_m * tiles_n;
+__device__ __forceinline__ int xcd_order(int total, int b) {
   const int xcd = b & 7, per = total >> 3, extra = total & 7;
-  const int id = xcd * per + (xcd < extra ? xcd : extra) + (b >> 3);
+  return xcd * per + (xcd < extra ? xcd : extra) + (b >> 3);
+}
+
+// Tile (tm, tn) at position id of a problem's raster.
+template <int BM, int BN>
+__device__ __forceinline__ void raster(int64_t M, int64_t N, int id, int& tm, int& tn) {
+  const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
   const int per_group = kGroupM * tiles_n;
   const int group = id / per_group;
   const int first_m = group * kGroupM;
@@ -264,6 +267,12 @@ __device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int b, int& tm
   const int in_group = id - group * per_group;
   tm = first_m + in_group % gsize;
   tn = in_group / gsize;
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int b, int& tm, int& tn) {
+  const int total = (int)((M + BM - 1) / BM) * (int)((N + BN - 1) / BN);
+  raster<BM, BN>(M, N, xcd_order(total, b), tm, tn);
 }
 
 // Quantized output: the tile's bf16 C, staged in LDS (row m at byte m *
@@ -325,7 +334,7 @@ __device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t
 // tile leaves as E4M3 codes and 1x128 scales of its bf16 values (see
 // store_quantized) instead of bf16.
 template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   constexpr int kWavesN = BN / WN;
   constexpr int kWaves = (BM / WM) * kWavesN;
   constexpr int TI = WM / 16, TJ = WN / 16;
@@ -353,8 +362,6 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   uint8_t* const scale_lds = lds + kStages * kStage;
   uint8_t* const dummy_lds = lds + kStages * kStage + kStages * kScaleStage;  // 256 bytes per wave
 
-  int tm, tn;
-  tile_coords<BM, BN>(g.M, g.N, blockIdx.x, tm, tn);
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63;
   const int wave = uniform(threadIdx.x >> 6);
@@ -826,6 +833,28 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 }
 
 template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
+  int tm, tn;
+  tile_coords<BM, BN>(g.M, g.N, blockIdx.x, tm, tn);
+  gemm_tile<PAIR, BM, BN, WM, WN, QOUT, FMT>(g, tm, tn);
+}
+
+// Grouped GEMM: one launch over several problems that share the pair, the
+// formats and K (the fused QKV or gate / up projections: one activation
+// operand, several weights and outputs).  The workgroups' XCD-ordered
+// positions run over the problems' rasters one after another; the problem
+// of a position is found from the prefix sums of the tile counts.
+template <int PAIR, int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_grouped_kernel(GemmGroup gs) {
+  const int id = xcd_order(gs.tile_start[gs.count], blockIdx.x);
+  int p = 0;
+  for (int i = 1; i < gs.count; ++i) p += id >= gs.tile_start[i] ? 1 : 0;
+  int tm, tn;
+  raster<BM, BN>(gs.prob[p].M, gs.prob[p].N, id - gs.tile_start[p], tm, tn);
+  gemm_tile<PAIR, BM, BN, WM, WN, false, 0>(gs.prob[p], tm, tn);
+}
+
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
 hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
@@ -934,6 +963,43 @@ FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 64, 64, 32, 32)
 #undef FP8Q_GEMM_KERNEL_FMT
 template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true, 0>(GemmArgs);
 template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true, 0>(GemmArgs);
+#define FP8Q_GEMM_GROUPED(PAIR)                                                  \
+  template __global__ void gemm_grouped_kernel<PAIR, 256, 256, 128, 64>(GemmGroup); \
+  template __global__ void gemm_grouped_kernel<PAIR, 128, 128, 64, 64>(GemmGroup);  \
+  template __global__ void gemm_grouped_kernel<PAIR, 64, 64, 32, 32>(GemmGroup);
+FP8Q_GEMM_GROUPED(kPairTensor)
+FP8Q_GEMM_GROUPED(kPairRow)
+FP8Q_GEMM_GROUPED(kPairBlock)
+#undef FP8Q_GEMM_GROUPED
+
+template <int PAIR, int BM, int BN, int WM, int WN>
+hipError_t launch_grouped_tiles(GemmGroup gs, hipStream_t s) {
+  int64_t total = 0;
+  for (int i = 0; i < gs.count; ++i) {
+    gs.tile_start[i] = (int)total;
+    total += ((gs.prob[i].M + BM - 1) / BM) * ((gs.prob[i].N + BN - 1) / BN);
+    if (total > 0x7fffffff) return hipErrorInvalidValue;
+  }
+  gs.tile_start[gs.count] = (int)total;
+  if (total <= 0) return hipErrorInvalidValue;
+  constexpr int threads = (BM / WM) * (BN / WN) * 64;
+  gemm_grouped_kernel<PAIR, BM, BN, WM, WN><<<dim3((unsigned)total), threads, 0, s>>>(gs);
+  return hipGetLastError();
+}
+
+// The tile size from the tile counts over all problems, as launch_pair
+// chooses it for one.
+template <int PAIR>
+hipError_t launch_grouped_pair(const GemmGroup& gs, hipStream_t s) {
+  int64_t big = 0, mid = 0;
+  for (int i = 0; i < gs.count; ++i) {
+    big += ((gs.prob[i].M + 255) / 256) * ((gs.prob[i].N + 255) / 256);
+    mid += ((gs.prob[i].M + 127) / 128) * ((gs.prob[i].N + 127) / 128);
+  }
+  if (big >= 512) return launch_grouped_tiles<PAIR, 256, 256, 128, 64>(gs, s);
+  if (mid >= 256) return launch_grouped_tiles<PAIR, 128, 128, 64, 64>(gs, s);
+  return launch_grouped_tiles<PAIR, 64, 64, 32, 32>(gs, s);
+}
 
 }  // namespace gemm_detail
 
@@ -958,6 +1024,23 @@ hipError_t launch_gemm(const GemmArgs& g, int pair, int formats, hipStream_t s) 
     case kPairBlock: return launch_formats<kPairBlock>(g, formats, s);
     case kPairBlockK: return launch_formats<kPairBlockK>(g, formats, s);
     case kPairBlockE8: return launch_split<kPairBlockE8, false, 0>(g, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_gemm_grouped(const GemmGroup& gs, int pair, hipStream_t s) {
+  if (gs.count < 1 || gs.count > kMaxGroup) return hipErrorInvalidValue;
+  // 32-bit operand offsets inside the kernel: each problem's A, B and C
+  // rows span less than 2 GiB
+  const int64_t lim = (int64_t)1 << 31;
+  for (int i = 0; i < gs.count; ++i) {
+    const GemmArgs& g = gs.prob[i];
+    if (g.M * g.lda >= lim || g.N * g.ldb >= lim || g.M * 2 * g.ldc >= lim) return hipErrorInvalidValue;
+  }
+  switch (pair) {
+    case kPairTensor: return launch_grouped_pair<kPairTensor>(gs, s);
+    case kPairRow: return launch_grouped_pair<kPairRow>(gs, s);
+    case kPairBlock: return launch_grouped_pair<kPairBlock>(gs, s);
     default: return hipErrorInvalidValue;
   }
 }

@@ -64,6 +64,19 @@ enum GemmPair { kPairTensor = 0, kPairRow = 1, kPairBlock = 2, kPairBlockK = 3, 
 // formats: bit 0 = A's codes are E5M2, bit 1 = B's (kPairBlock and
 // kPairBlockK only; 0 for E4M3 x E4M3).
 hipError_t launch_gemm(const GemmArgs& g, int pair, int formats, hipStream_t s);
+
+// Grouped GEMM: up to kMaxGroup problems of one pair (tensor, row or
+// 1x128 x 128x128) and one K in one launch; tile_start is filled by the
+// launcher (prefix sums of the tile counts).
+constexpr int kMaxGroup = 8;
+struct GemmGroup {
+  GemmArgs prob[kMaxGroup];
+  int tile_start[kMaxGroup + 1];
+  int count;
+};
+// The same 32-bit offset limits as launch_gemm's sub-problems, per problem
+// (else hipErrorInvalidValue; the C-ABI checks them first).
+hipError_t launch_gemm_grouped(const GemmGroup& gs, int pair, hipStream_t s);
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s);
 
 // Calibrated Clipping: per-token float32 arrays of n tokens, the grids

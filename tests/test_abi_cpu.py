@@ -140,6 +140,29 @@ def test_scales_count_pow2_and_e5m2_flags(L):
     assert L.fp8q_scales_count(256, 384, fp8q.BLOCK_1x128, 8) == -1
 
 
+def grouped(L, probs, gA=3, gB=5, K=256, count=None):
+    arr = (fp8q.GemmProblem * max(1, len(probs)))()
+    for i, kw in enumerate(probs):
+        d = dict(A=FAKE, sA=FAKE, lda=256, B=FAKE, sB=FAKE, ldb=256, C=FAKE, ldc=512, M=256, N=512)
+        d.update(kw)
+        arr[i] = fp8q.GemmProblem(**d)
+    return L.fp8q_gemm_grouped(arr, len(probs) if count is None else count, gA, gB, K, None)
+
+
+def test_gemm_grouped_rejections(L):
+    assert L.fp8q_gemm_grouped(None, 1, 3, 5, 256, None) == -1
+    assert grouped(L, [{}], count=0) == -1
+    assert grouped(L, [{}] * 9) == -1                        # more than FP8Q_MAX_GROUP
+    assert grouped(L, [{}, dict(B=None)]) == -1              # a bad second problem
+    assert grouped(L, [{}, dict(M=0)]) == -1
+    assert grouped(L, [{}, dict(ldc=256)]) == -1             # ldc < N
+    assert grouped(L, [{}], gA=3, gB=3) == -2                # the wgrad pair is not grouped
+    assert grouped(L, [{}], K=200) == -2
+    assert grouped(L, [{}, dict(N=200, ldc=256)]) == -2      # 128x128 B needs N % 128
+    assert grouped(L, [dict(M=1 << 24, lda=256)]) == -2      # A spans 4 GiB
+    assert grouped(L, [{}, dict(C=FAKE + 2)]) == -3
+
+
 def gemm_f(L, formats, **kw):
     args = dict(A=FAKE, sA=FAKE, gA=3, lda=256, B=FAKE, sB=FAKE, gB=5, ldb=256, M=256, N=256, K=256)
     args.update(kw)
