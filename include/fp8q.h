@@ -109,7 +109,11 @@ int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g,
  * and 128x128) must be a multiple of 128 (else FP8Q_ERR_UNSUPPORTED).
  * Alignment: x and codes 16-byte aligned, ldx % 8 == 0, ldc % 16 == 0,
  * scales 4-byte aligned (else FP8Q_ERR_ALIGN).
- * TENSOR, ROW and COL use `scales` as their amax scratch between kernels.
+ * TENSOR, COL and ROW with FP8Q_OUT_TRANSPOSED run three kernels (partial
+ * amaxes, their reduction to S, the cast) and keep the partial amaxes in
+ * `codes` between them (only the codes' own bytes, never the padding of a
+ * strided code array), or in `scales` when each unit has one partial; the
+ * cast then overwrites them.
  */
 fp8q_status fp8q_quantize(const void *x, int64_t rows, int64_t cols,
                           int64_t ldx, fp8q_granularity g, unsigned flags,

@@ -22,14 +22,15 @@ FLAGS = [
 
 
 def check_no_scratch(src, remarks):
-    """The GEMM kernels read LDS with inline asm whose results are only valid
-    after an explicit wait; a register spill could copy such a value early.
-    Refuse a build in which any GEMM kernel uses scratch memory."""
+    """The tiled GEMM kernels read LDS with inline asm whose results are only
+    valid after an explicit wait; a register spill could copy such a value
+    early (and a spill in any GEMM kernel costs its memory path).  Refuse a
+    build in which any GEMM kernel uses scratch memory."""
     name = None
     for line in remarks.splitlines():
         if "Function Name:" in line:
             name = line.split("Function Name:")[1].split()[0]
-        elif "ScratchSize [bytes/lane]:" in line and name and "gemm_kernel" in name:
+        elif "ScratchSize [bytes/lane]:" in line and name and "gemm" in name:
             size = int(line.split("ScratchSize [bytes/lane]:")[1].split()[0])
             if size != 0:
                 raise RuntimeError("%s: %s spills to scratch (%d bytes per lane)" % (src, name, size))

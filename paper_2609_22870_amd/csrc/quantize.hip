@@ -8,10 +8,13 @@
 // 1x128 amax a four-step DPP reduction; 128x1 and 128x128 amaxes add a
 // cross-row shuffle and one LDS exchange between the four waves.
 //
-// Granularities whose units span several tiles (tensor, row, column) run in
-// two passes: an amax pass that max-reduces into the scale array with 32-bit
-// atomics on the fp32 bit patterns (non-negative floats order like their
-// bits), then the cast pass, then a small pass that turns each amax into S.
+// Granularities whose units span several tiles (tensor, column, and row with
+// transposed output) run in three kernels: an amax pass in which every
+// workgroup writes its own partial maxima (no atomics: thousands of them on
+// one address serialize), a small pass that reduces the partials of each
+// unit to its S, and the cast pass.  The partials live in the caller's code
+// array, which the cast overwrites afterwards (in `scales` when each unit
+// has a single partial).
 #include "device_common.h"
 #include "internal.h"
 
@@ -139,15 +142,19 @@ __device__ __forceinline__ void encode_patch(const Tile& t, const float (&su)[8]
     encode_all([](float x, float s_, float r_) { return slow_quotient(x, s_, r_); });
 }
 
+// The per-unit constants of a unit whose S is known (the cast pass of the
+// multi-tile granularities): the same values unit_scale gives for its amax.
+__device__ __forceinline__ UnitScale unit_of_scale(float s) { return UnitScale{s, 1.0f / s, s >= 0x1p-90f}; }
+
 // Per-unit scales when a thread's eight rows are eight units shared by the
 // 16 lanes of its DPP row: lane cc of the row group holds the amax of row
 // cc % 8, computes that unit's S and 1/S (two IEEE divisions), and the
 // group exchanges them by lane shuffles.
-template <bool E5>
+template <bool E5, bool KNOWN = false>
 __device__ __forceinline__ void share_row_units(float amax, bool pow2, UnitScale& mine, float (&su)[8],
                                                 float (&ru)[8]) {
   const int lane = threadIdx.x & 63;
-  mine = unit_scale_fmt<E5>(amax, pow2);
+  mine = KNOWN ? unit_of_scale(amax) : unit_scale_fmt<E5>(amax, pow2);
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     su[i] = __shfl(mine.s, (lane & 48) | i, 64);
@@ -159,11 +166,11 @@ __device__ __forceinline__ void share_row_units(float amax, bool pow2, UnitScale
 // (rg < 8, cc) holds the amax of column 8 cc + rg, computes its S and 1/S,
 // and the block exchanges them through LDS (the upper half of lds_red, after
 // every read of its lower half).
-template <bool E5>
+template <bool E5, bool KNOWN = false>
 __device__ __forceinline__ void share_col_units(float amax, bool pow2, float* lds_red, UnitScale& mine,
                                                 float (&su)[8], float (&ru)[8]) {
   const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
-  mine = unit_scale_fmt<E5>(amax, pow2);
+  mine = KNOWN ? unit_of_scale(amax) : unit_scale_fmt<E5>(amax, pow2);
   float2* lds_su = reinterpret_cast<float2*>(lds_red + 2 * kTile);
   __syncthreads();
   if (rg < 8) lds_su[cc * 8 + rg] = make_float2(mine.s, mine.r);
@@ -272,14 +279,14 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
   UnitScale mine;  // the unit this thread computes (eight-unit case)
   float su[8], ru[8];
   if (by_row) {
-    float amax;
     if (K == kBlock1x128) {
-      amax = block_row_amax(t);
+      const float amax = block_row_amax(t);
+      share_row_units<E5>(amax, a.pow2 != 0, mine, su, ru);
     } else {
+      // ROW with transposed output: S of each row, from the reduce pass
       const int64_t r = row0 + (cc & 7);
-      amax = r < a.rows ? a.scales[r] : 0.0f;
+      share_row_units<E5, true>(r < a.rows ? a.scales[r] : 1.0f, false, mine, su, ru);
     }
-    share_row_units<E5>(amax, a.pow2 != 0, mine, su, ru);
   } else if (by_col) {
     float amax;
     if (K == kBlock128x1) {
@@ -288,13 +295,15 @@ __global__ __launch_bounds__(kThreads) void quant_tile_kernel(QuantArgs a) {
       amax = m[0];
 #pragma unroll
       for (int j = 1; j < 8; ++j) amax = (rg & 7) == j ? m[j] : amax;
+      share_col_units<E5>(amax, a.pow2 != 0, lds_red, mine, su, ru);
     } else {
+      // COL: S of each column, from the reduce pass
       const int64_t cj = c0 + cc * 8 + (rg & 7);
-      amax = cj < a.cols ? a.scales[cj] : 0.0f;
+      share_col_units<E5, true>(cj < a.cols ? a.scales[cj] : 1.0f, false, lds_red, mine, su, ru);
     }
-    share_col_units<E5>(amax, a.pow2 != 0, lds_red, mine, su, ru);
   } else {
-    mine = unit_scale_fmt<E5>(K == kBlock128x128 ? tile_max(t, lds_red) : a.scales[0], a.pow2 != 0);
+    // 128x128: the tile's amax; TENSOR: S from the reduce pass
+    mine = K == kBlock128x128 ? unit_scale_fmt<E5>(tile_max(t, lds_red), a.pow2 != 0) : unit_of_scale(a.scales[0]);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       su[i] = mine.s;
@@ -373,34 +382,79 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
 
 // Amax pass of the two-pass granularities: atomic max of |x| into `scales`
 // (zeroed beforehand) per tensor, row or column.
+// Partial maxima of the multi-tile granularities: float i sits at float
+// i % per of line i / per, lines being `ld` bytes apart.  In the code array
+// a line is one of its rows (columns when transposed) and holds per = its
+// length / 4 floats, so nothing outside the codes themselves is written; in
+// `scales` (one partial per unit) it is one line.
+struct Partials {
+  uint8_t* base;
+  int64_t per, ld;
+  __device__ __forceinline__ float* at(int64_t i) const {
+    return reinterpret_cast<float*>(base + (i / per) * ld) + (i % per);
+  }
+};
+
+// Amax pass of COL and of ROW with transposed output, per 128 x 128 tile:
+// the partial of row r in tile column tc at tc * rows + r, of column c in
+// tile row tr at tr * cols + c.
 template <int K>
-__global__ __launch_bounds__(kThreads) void amax_tile_kernel(QuantArgs a) {
+__global__ __launch_bounds__(kThreads) void amax_tile_kernel(QuantArgs a, Partials part) {
   __shared__ float lds_red[4 * kTile];
   const int cc = threadIdx.x & 15, rg = threadIdx.x >> 4;
   const int64_t r0 = (int64_t)blockIdx.y * kTile;
   const int64_t c0 = (int64_t)blockIdx.x * kTile;
   Tile t;
   load_patch(a, r0 + rg * 8, c0 + cc * 8, t);
-  unsigned int* bits = reinterpret_cast<unsigned int*>(a.scales);
   if (K == kPreRow) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float m = row16_max(row_partial_max(t, i));
       const int64_t r = r0 + rg * 8 + i;
-      if (cc == 0 && r < a.rows) atomicMax(bits + r, __float_as_uint(m));
-    }
-  } else if (K == kPreCol) {
-    float m[8];
-    tile_col_max(t, lds_red, m);
-    const int64_t c = c0 + cc * 8;
-    if (rg == 0 && c < a.cols) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) atomicMax(bits + c + j, __float_as_uint(m[j]));
+      if (cc == 0 && r < a.rows) *part.at((int64_t)blockIdx.x * a.rows + r) = m;
     }
   } else {
-    const float m = tile_max(t, lds_red);
-    if (threadIdx.x == 0) atomicMax(bits, __float_as_uint(m));
+    float m[8];
+    tile_col_max(t, lds_red, m);
+    const int64_t c = c0 + cc * 8;  // cols % 16 == 0: all eight columns or none
+    if (rg == 0 && c < a.cols) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) *part.at((int64_t)blockIdx.y * a.cols + c + j) = m[j];
+    }
   }
+}
+
+// S of each unit from its partials (those of unit u at u, u + units, ...):
+// a workgroup takes 64 units, its four waves split the partials, and LDS
+// joins the waves.
+template <bool E5>
+__global__ __launch_bounds__(256) void reduce_units_kernel(Partials part, int64_t units, int64_t nparts,
+                                                          float* scales, int pow2) {
+  __shared__ float lds[4][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t u = (int64_t)blockIdx.x * 64 + lane;
+  float m = 0.0f;
+  if (u < units)
+    for (int64_t p = wave; p < nparts; p += 4) m = fmaxf(m, *part.at(p * units + u));
+  lds[wave][lane] = m;
+  __syncthreads();
+  if (wave == 0 && u < units) {
+    m = fmaxf(fmaxf(lds[0][lane], lds[1][lane]), fmaxf(lds[2][lane], lds[3][lane]));
+    scales[u] = unit_scale_fmt<E5>(m, pow2 != 0).s;
+  }
+}
+
+// S of TENSOR from the nparts partials of its amax pass (one workgroup).
+template <bool E5>
+__global__ __launch_bounds__(256) void reduce_tensor_kernel(Partials part, int64_t nparts, float* scales, int pow2) {
+  __shared__ float lds4[4];
+  float m = 0.0f;
+  for (int64_t p = threadIdx.x; p < nparts; p += 256) m = fmaxf(m, *part.at(p));
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    scales[0] = unit_scale_fmt<E5>(fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3])), pow2 != 0).s;
 }
 
 // ROW units without transposition, in one pass over memory: a wave takes
@@ -470,10 +524,9 @@ __global__ __launch_bounds__(kRowWaves * 64) void quant_row_kernel(QuantArgs a) 
 }
 
 // Amax pass of TENSOR: a grid-stride walk over 32 x 512 tiles (1 KB row
-// pieces per load instruction) keeping a running max per thread, then one
-// atomic max per workgroup (an atomic per tile would queue thousands of
-// them on the one address).
-__global__ __launch_bounds__(kThreads) void amax_tensor_kernel(QuantArgs a) {
+// pieces per load instruction) keeping a running max per thread; workgroup
+// b writes its maximum as partial b.
+__global__ __launch_bounds__(kThreads) void amax_tensor_kernel(QuantArgs a, Partials part) {
   __shared__ float lds4[4];
   const int64_t tiles_c = (a.cols + kWideCols - 1) / kWideCols;
   const int64_t tiles = tiles_c * ((a.rows + kWideRows - 1) / kWideRows);
@@ -488,21 +541,7 @@ __global__ __launch_bounds__(kThreads) void amax_tensor_kernel(QuantArgs a) {
   m = wave_max(m);
   if ((threadIdx.x & 63) == 0) lds4[threadIdx.x >> 6] = m;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    m = fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3]));
-    atomicMax(reinterpret_cast<unsigned int*>(a.scales), __float_as_uint(m));
-  }
-}
-
-__global__ void fill_zero_kernel(float* p, int64_t n) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = 0.0f;
-}
-
-template <bool E5>
-__global__ void amax_to_scale_kernel(float* p, int64_t n, int pow2) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
-    p[i] = unit_scale_fmt<E5>(p[i], pow2 != 0).s;
+  if (threadIdx.x == 0) *part.at(blockIdx.x) = fmaxf(fmaxf(lds4[0], lds4[1]), fmaxf(lds4[2], lds4[3]));
 }
 
 template <bool E5>
@@ -522,41 +561,56 @@ hipError_t launch_tile(const QuantArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// Workgroups of the TENSOR amax pass (each writes one partial).
+constexpr int64_t kTensorParts = 1024;
+
+// TENSOR, COL and ROW with transposed output: partial amaxes, their
+// reduction to S, then the cast.
 template <int K, bool E5>
-hipError_t launch_two_pass(const QuantArgs& a, bool trans, int64_t nscales, hipStream_t s) {
-  const unsigned fill_blocks = (unsigned)((nscales + 255) / 256 < 4096 ? (nscales + 255) / 256 : 4096);
-  fill_zero_kernel<<<fill_blocks, 256, 0, s>>>(a.scales, nscales);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+hipError_t launch_two_pass(const QuantArgs& a, bool trans, hipStream_t s) {
+  // the code array as lines of floats (rows % 16 == 0 when transposed,
+  // cols % 16 == 0 always)
+  Partials in_codes{a.codes, (trans ? a.rows : a.cols) / 4, a.ldc};
+  Partials in_scales{reinterpret_cast<uint8_t*>(a.scales), INT64_MAX, 0};
+  hipError_t e;
   if (K == kPreTensor) {
     const int64_t tiles = ((a.cols + kWideCols - 1) / kWideCols) * ((a.rows + kWideRows - 1) / kWideRows);
-    amax_tensor_kernel<<<(unsigned)(tiles < 2048 ? tiles : 2048), kThreads, 0, s>>>(a);
+    const int64_t parts = tiles < kTensorParts ? tiles : kTensorParts;  // <= rows * cols / 4: they fit
+    amax_tensor_kernel<<<(unsigned)parts, kThreads, 0, s>>>(a, in_codes);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    reduce_tensor_kernel<E5><<<1, 256, 0, s>>>(in_codes, parts, a.scales, a.pow2);
   } else {
-    const dim3 grid((unsigned)((a.cols + kTile - 1) / kTile), (unsigned)((a.rows + kTile - 1) / kTile));
-    amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a);
+    const int64_t tiles_r = (a.rows + kTile - 1) / kTile, tiles_c = (a.cols + kTile - 1) / kTile;
+    const int64_t units = K == kPreRow ? a.rows : a.cols, nparts = K == kPreRow ? tiles_c : tiles_r;
+    // one partial per unit: in place in `scales`; else nparts <= (its
+    // dimension) / 4 (it exceeds 128 and so 4 nparts), and the codes hold
+    // rows * cols / 4 floats
+    const Partials part = nparts == 1 ? in_scales : in_codes;
+    const dim3 grid((unsigned)tiles_c, (unsigned)tiles_r);
+    amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a, part);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    reduce_units_kernel<E5><<<(unsigned)((units + 63) / 64), 256, 0, s>>>(part, units, nparts, a.scales, a.pow2);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  e = trans ? launch_tile<K, true, E5>(a, s) : launch_tile<K, false, E5>(a, s);
-  if (e != hipSuccess) return e;
-  amax_to_scale_kernel<E5><<<fill_blocks, 256, 0, s>>>(a.scales, nscales, a.pow2);
-  return hipGetLastError();
+  return trans ? launch_tile<K, true, E5>(a, s) : launch_tile<K, false, E5>(a, s);
 }
 
 template <bool E5>
 hipError_t launch_quantize_fmt(const QuantArgs& a, int granularity, bool trans, int64_t nscales, hipStream_t s) {
+  (void)nscales;
   switch (granularity) {
     case 3: return trans ? launch_tile<kBlock1x128, true, E5>(a, s) : launch_tile<kBlock1x128, false, E5>(a, s);
     case 4: return trans ? launch_tile<kBlock128x1, true, E5>(a, s) : launch_tile<kBlock128x1, false, E5>(a, s);
     case 5:
       return trans ? launch_tile<kBlock128x128, true, E5>(a, s) : launch_tile<kBlock128x128, false, E5>(a, s);
-    case 0: return launch_two_pass<kPreTensor, E5>(a, trans, nscales, s);
+    case 0: return launch_two_pass<kPreTensor, E5>(a, trans, s);
     case 1: {
-      if (trans) return launch_two_pass<kPreRow, E5>(a, trans, nscales, s);
+      if (trans) return launch_two_pass<kPreRow, E5>(a, trans, s);
       const int64_t blocks = (a.rows + kRowWaves - 1) / kRowWaves;
       quant_row_kernel<E5><<<(unsigned)(blocks < 16384 ? blocks : 16384), kRowWaves * 64, 0, s>>>(a);
       return hipGetLastError();
     }
-    case 2: return launch_two_pass<kPreCol, E5>(a, trans, nscales, s);
+    case 2: return launch_two_pass<kPreCol, E5>(a, trans, s);
     default: return hipErrorInvalidValue;
   }
 }

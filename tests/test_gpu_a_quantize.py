@@ -80,6 +80,26 @@ def test_padded_leading_dimensions():
     assert torch.all(codes[:, 512:] == 0x5A)  # padding untouched
 
 
+@pytest.mark.parametrize("g,transposed", [(fp8q.TENSOR, False), (fp8q.TENSOR, True), (fp8q.COL, False),
+                                           (fp8q.COL, True), (fp8q.ROW, True)])
+def test_padded_codes_multi_tile(g, transposed):
+    """TENSOR, COL and transposed ROW keep their partial amaxes in the code
+    array between passes: only the codes' own bytes may be written, never
+    the padding between rows of a strided code array."""
+    rows, cols = 400, 528  # several tiles each way, ragged
+    x = synth.activations(rows, cols, seed=41 + g, outlier_seed=42 + g)
+    lines, length = (cols, rows) if transposed else (rows, cols)
+    buf = torch.full((lines, length + 48), 0x5A, dtype=torch.uint8, device=DEV)
+    cview = buf[:, :length]
+    scales = torch.empty(fp8q.scales_count(rows, cols, g, transposed), dtype=torch.float32, device=DEV)
+    fp8q.quantize(x.to(DEV), g, transposed, codes=cview, scales=scales)
+    torch.cuda.synchronize()
+    oc, os_ = _par.quantize(synth.bf16_bits(x), g, transposed)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint32), os_.view(np.uint32))
+    assert np.array_equal(cview.cpu().numpy(), oc)
+    assert torch.all(buf[:, length:] == 0x5A)
+
+
 def test_special_blocks():
     """All-zero, signed-zero, single-nonzero, constant-magnitude and
     subnormal-amax blocks, each a 1x128 block of one row."""

@@ -41,14 +41,23 @@ def oracle_operand(x, g, transposed=False):
     return _par.quantize(synth.bf16_bits(x), g, transposed)
 
 
-def run_pair(a_src, b_src, ga, gb, a_t=False, b_t=False, rows=None, label=""):
+def run_pair(a_src, b_src, ga, gb, a_t=False, b_t=False, rows=None, label="", pad=0):
     """a_src, b_src: bf16 CUDA tensors whose quantization (optionally
     transposed) gives A [M, K] and B [N, K].  Checks the listed rows of C (all
-    rows by default) against the oracle; returns the error."""
+    rows by default) against the oracle; returns the error.  pad > 0: C is
+    the first N columns of a [M, N + pad] buffer whose other columns must
+    stay untouched."""
     print("gemm parity", label, tuple(a_src.shape), tuple(b_src.shape), ga, gb, flush=True)
     A, sA = gpu_operand(a_src, ga if not a_t else fp8q.BLOCK_128x1, a_t)
     B, sB = gpu_operand(b_src, gb if not b_t else (fp8q.BLOCK_128x1 if gb == fp8q.BLOCK_1x128 else gb), b_t)
-    C = fp8q.gemm(A, sA, ga, B, sB, gb)
+    if pad:
+        buf = torch.full((A.shape[0], B.shape[0] + pad), -7.0, dtype=torch.bfloat16, device=DEV)
+        C = fp8q.gemm(A, sA, ga, B, sB, gb, out=buf[:, :B.shape[0]])
+        torch.cuda.synchronize()
+        assert torch.all(buf[:, B.shape[0]:] == -7.0), "columns past N were written"
+        del buf
+    else:
+        C = fp8q.gemm(A, sA, ga, B, sB, gb)
     torch.cuda.synchronize()
     M = A.shape[0]
     if rows is None:
@@ -85,6 +94,20 @@ def test_small_all_pairs(pair):
     a = synth.activations(M, K, seed=101, outlier_seed=102, device=DEV)
     b = synth.weights(N, K, seed=103, device=DEV)
     run_pair(a, b, ga, gb, label=pair)
+
+
+@pytest.mark.parametrize("pair", ["tensor", "row"])
+@pytest.mark.parametrize("M,K,N", [(200, 256, 390), (16384 + 96, 128, 8192 + 6)])
+def test_ragged_columns_padded_output(pair, M, K, N):
+    """N not a multiple of 4, so the last lane holding columns of a row has
+    some of its four past N: those stay untouched in a padded output, the
+    rest match the oracle.  The large shape runs the 256 x 256 kernel with a
+    ragged last tile row and tile column (sampled rows plus the last ones)."""
+    ga, gb = PAIRS[pair]
+    a = synth.activations(M, K, seed=151, outlier_seed=152, device=DEV)
+    b = synth.weights(N, K, seed=153, device=DEV)
+    rows = None if M < 1024 else np.unique(np.concatenate([_par.sample_rows(M), np.arange(M - 20, M)]))
+    run_pair(a, b, ga, gb, rows=rows, label="ragged columns " + pair, pad=6)
 
 
 def test_tiny_tensorwise_workload():
