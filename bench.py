@@ -157,7 +157,10 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
       (16384 x 25600 -> 5120) with dY's codes in E5M2 against E4M3;
     * the grouped GEMM of the fused projections of the step's X (query, key
       and value: 4096 + 1024 + 1024 outputs; gate and up: 2 x 12288) in one
-      launch, against one fp8q_gemm call per projection."""
+      launch, against one fp8q_gemm call per projection;
+    * the paper's three scaling recipes on the step's layer (tensorwise,
+      rowwise: per-token X and per-output-channel W, blockwise): quantize X,
+      quantize W and the GEMM, each timed."""
     rows, cols = 16384, 25600
     dy = synth.grads(rows, cols, seed=synth.seed_for(5, 2), device=dev)
     outs = fp8q.quantize_dual(dy)
@@ -215,6 +218,24 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
     pow2_tflops = 2.0 * M * N * K / (t_pow2 * 1e-6) / 1e12
     del y, xb, sxb, wb, swb
 
+    # the paper's three scaling recipes on the step's layer: quantize X,
+    # quantize W, GEMM
+    recipes = {}
+    for name, gx, gw in (("tensorwise", fp8q.TENSOR, fp8q.TENSOR), ("rowwise", fp8q.ROW, fp8q.ROW),
+                         ("blockwise", fp8q.BLOCK_1x128, fp8q.BLOCK_128x128)):
+        xa, sxa = fp8q.quantize(x, gx)
+        wa, swa = fp8q.quantize(w, gw)
+        ya = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        t_x = timed(lambda: fp8q.quantize(x, gx, codes=xa, scales=sxa))
+        t_w = timed(lambda: fp8q.quantize(w, gw, codes=wa, scales=swa))
+        t_g = timed(lambda: fp8q.gemm(xa, sxa, gx, wa, swa, gw, out=ya))
+        step = t_x + t_w + t_g
+        recipes[name] = {"quantize_x_us": round(t_x, 1), "quantize_w_us": round(t_w, 1), "gemm_us": round(t_g, 1),
+                         "step_us": round(step, 1),
+                         "step_tflops": round(2.0 * M * N * K / (step * 1e-6) / 1e12, 1),
+                         "gemm_tflops": round(2.0 * M * N * K / (t_g * 1e-6) / 1e12, 1)}
+        del xa, sxa, wa, swa, ya
+
     grouped = {}
     for kind, widths in (("qkv", (4096, 1024, 1024)), ("gate_up", (12288, 12288))):
         probs = []
@@ -257,6 +278,7 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
         "dgrad_e5m2_us": round(t_dg5, 1), "dgrad_e5m2_tflops": round(dg_flops / (t_dg5 * 1e-6) / 1e12, 1),
         "dgrad_e4m3_us": round(t_dg4, 1), "dgrad_e4m3_tflops": round(dg_flops / (t_dg4 * 1e-6) / 1e12, 1)},
         "gemm_grouped_8b_fused_projections": grouped,
+        "scaling_recipes_8b_ffn_up": recipes,
         "calibrated_clipping_grpo_batch": {
         "tokens": ntok, "us": round(t_clip, 1), "gbs": round(clip_gbs, 1),
         "frac_hbm": round(clip_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": round(clip_bytes)}}
