@@ -284,6 +284,69 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
         "frac_hbm": round(clip_gbs / PEAK_HBM_GBS, 4), "algorithmic_bytes": round(clip_bytes)}}
 
 
+def clock_under_load(torch, f, seconds=1.0):
+    """Shader clock and socket power while f (one GEMM launch) runs back to
+    back for about `seconds`, sampled every 10 ms from the GPU metrics table
+    through amdsmi in a second thread; with the GEMM's event-timed average
+    over the same period.  None when amdsmi is not importable or the device
+    is not found."""
+    import threading
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+    except Exception as e:  # the metric is optional: report why it is missing
+        return {"error": "amdsmi: %s" % e}
+    try:
+        handles = amdsmi.amdsmi_get_processor_handles()
+        h = handles[0] if len(handles) == 1 else None
+        if h is None:
+            bus = getattr(torch.cuda.get_device_properties(0), "pci_bus_id", None)
+            for c in handles:
+                if bus is not None and int(amdsmi.amdsmi_get_gpu_device_bdf(c).split(":")[1], 16) == bus:
+                    h = c
+        if h is None:
+            return {"error": "device not matched among %d" % len(handles)}
+        clocks, power, stop = [], [], threading.Event()
+
+        def poll():
+            while not stop.is_set():
+                m = amdsmi.amdsmi_get_gpu_metrics_info(h)
+                xcd = [v for v in m.get("current_gfxclks", []) if isinstance(v, int) and 0 < v < 10000]
+                if xcd:
+                    clocks.append(sum(xcd) / len(xcd))
+                p = m.get("current_socket_power")
+                if isinstance(p, (int, float)) and 0 < p < 5000:
+                    power.append(float(p))
+                stop.wait(0.01)
+
+        th = threading.Thread(target=poll, daemon=True)
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        th.start()
+        t0, n = time.perf_counter(), 0
+        s.record()
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(10):
+                f()
+            n += 10
+            torch.cuda.synchronize()
+        e.record()
+        torch.cuda.synchronize()
+        stop.set()
+        th.join()
+        med = lambda v: sorted(v)[len(v) // 2] if v else None
+        return {"gfx_mhz_median": med(clocks), "gfx_mhz_min": min(clocks) if clocks else None,
+                "gfx_mhz_max": max(clocks) if clocks else None, "socket_power_w_median": med(power),
+                "samples": len(clocks), "gemm_us": round(s.elapsed_time(e) / n * 1000.0, 1), "launches": n}
+    except Exception as e:
+        return {"error": "amdsmi: %s" % e}
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -340,6 +403,8 @@ def main():
     qx_ms = sum(e[0].elapsed_time(e[1]) for e in events) / args.steps
     qw_ms = sum(e[1].elapsed_time(e[2]) for e in events) / args.steps
     gemm_ms = sum(e[2].elapsed_time(e[3]) for e in events) / args.steps
+    gemm_sorted = sorted(e[2].elapsed_time(e[3]) for e in events)
+    pct = lambda q: round(gemm_sorted[min(len(gemm_sorted) - 1, int(q * len(gemm_sorted)))] * 1000.0, 1)
 
     flops = 2.0 * M * N * K
     value = flops / (ms_step * 1e-3) / 1e12
@@ -375,8 +440,17 @@ def main():
         "quantize_gbs": {"x_1x128": round(qx_bytes / (qx_ms * 1e-3) / 1e9, 1),
                          "w_128x128": round(qw_bytes / (qw_ms * 1e-3) / 1e9, 1),
                          "hbm_peak": PEAK_HBM_GBS},
+        "gemm_us_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
         "timed_wall_s": round(wall, 3),
     }
+    # the shader clock the GEMM runs at: its peak at that clock is the
+    # dense FP8 rate scaled by clock / 2400 MHz
+    clk = clock_under_load(torch, lambda: fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y))
+    if clk and clk.get("gfx_mhz_median"):
+        t = flops / (clk["gemm_us"] * 1e-6) / 1e12
+        clk["gemm_tflops"] = round(t, 1)
+        clk["frac_of_peak_at_this_clock"] = round(t / (PEAK_FP8_TFLOPS * clk["gfx_mhz_median"] / 2400.0), 4)
+    out["clock_under_gemm"] = clk
     if args.calibrate_copy_mib > 0:
         n = args.calibrate_copy_mib << 20
         src = torch.zeros(n, dtype=torch.uint8, device=dev)
