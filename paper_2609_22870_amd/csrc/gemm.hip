@@ -333,10 +333,15 @@ __device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t
 // each owning WM x WN as (WM/16) x (WN/16) MFMA tiles of 16 x 16.  QOUT: the
 // tile leaves as E4M3 codes and 1x128 scales of its bf16 values (see
 // store_quantized) instead of bf16.
-template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
+// KS > 1 (skinny problems, 64 x 64 tiles): KS groups of waves share the
+// tile, group k taking the K blocks k, k + KS, ... with its own LDS ring;
+// their partial tiles are summed in LDS at the end, group 1 into group 0,
+// then group 2, ... (a fixed order).  Each group's step chain (barrier,
+// fragment reads, MFMAs, FMAs) then overlaps the others' on the same SIMDs.
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT, int KS = 1>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   constexpr int kWavesN = BN / WN;
-  constexpr int kWaves = (BM / WM) * kWavesN;
+  constexpr int kWaves = (BM / WM) * kWavesN;  // waves of one group
   constexpr int TI = WM / 16, TJ = WN / 16;
   constexpr int kTileA = BM * kBK, kTileB = BN * kBK, kStage = kTileA + kTileB;
   // kBlockScaled: per-K-step scale vectors are staged with the tiles;
@@ -358,15 +363,21 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   // second workgroup per CU); the 64 x 64 tile of skinny problems, whose
   // steps are short next to the load latency, keeps four.
   constexpr int kStages = BM >= 128 ? 2 : 4;
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStage + kStages * kScaleStage + kWaves * 256];
+  static_assert(KS == 1 || (kStages > 2 && !QOUT), "K groups: the 64 x 64 tile");
+  constexpr int kGroupBytes = kStages * kStage + kStages * kScaleStage;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_all[KS * kGroupBytes + KS * kWaves * 256];
+  const int wave_all = uniform(threadIdx.x >> 6);
+  const int kg = KS > 1 ? uniform(wave_all / kWaves) : 0;  // K group
+  uint8_t* const lds = lds_all + kg * kGroupBytes;
   uint8_t* const scale_lds = lds + kStages * kStage;
-  uint8_t* const dummy_lds = lds + kStages * kStage + kStages * kScaleStage;  // 256 bytes per wave
+  uint8_t* const dummy_lds = lds_all + KS * kGroupBytes;  // 256 bytes per wave
 
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
   const int lane = threadIdx.x & 63;
-  const int wave = uniform(threadIdx.x >> 6);
+  const int wave = KS > 1 ? uniform(wave_all % kWaves) : wave_all;  // within the group
   const int wm = (wave / kWavesN) * WM, wn = (wave % kWavesN) * WN;
-  const int KT = (int)(g.K / kBK);
+  const int KT = (int)(g.K / kBK) / KS;  // steps of this group (KS divides K / 128)
+  auto kb = [&](int st) { return st * KS + kg; };  // K block of the group's step st
   const int mw = (int)m0 + wm, nw = (int)n0 + wn;  // wave's first row / column
 
   v4f acc[TI][TJ];
@@ -417,7 +428,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   };
   scale_offsets();
   // LDS destination of this wave's instruction: stage st's scale vectors
-  uint8_t* const q_to = wave < kQ ? scale_lds + q_dst : dummy_lds + wave * 256;
+  uint8_t* const q_to = wave < kQ ? scale_lds + q_dst : dummy_lds + wave_all * 256;
   const int q_stride = uniform(wave < kQ ? kScaleStage : 0);
   auto load_scales = [&](int kt, int st) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs_q, (lds_void*)(q_to + st * q_stride), 4, q_voff,
@@ -431,15 +442,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   auto prologue = [&]() {
     if constexpr (kStages == 2) {
       // stage 0, then stage 1's B tile (see the schedule below)
-      if constexpr (kBlockScaled) load_scales(0, 0);
-      ldA.load(0, lds, wave);
-      ldB.load(0, lds + kTileA, wave);
-      if (KT > 1) ldB.load(kBK, lds + kStage + kTileA, wave);
+      if constexpr (kBlockScaled) load_scales(kb(0), 0);
+      ldA.load(kb(0) * kBK, lds, wave);
+      ldB.load(kb(0) * kBK, lds + kTileA, wave);
+      if (KT > 1) ldB.load(kb(1) * kBK, lds + kStage + kTileA, wave);
     } else {
       for (int st = 0; st < kStages - 1 && st < KT; ++st) {
-        if constexpr (kBlockScaled) load_scales(st, st);
-        ldA.load(st * kBK, lds + st * kStage, wave);
-        ldB.load(st * kBK, lds + st * kStage + kTileA, wave);
+        if constexpr (kBlockScaled) load_scales(kb(st), st);
+        ldA.load(kb(st) * kBK, lds + st * kStage, wave);
+        ldB.load(kb(st) * kBK, lds + st * kStage + kTileA, wave);
       }
     }
   };
@@ -490,8 +501,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
     uint8_t* cur = lds + cur_st * kStage;
     uint8_t* cur_scales = scale_lds + cur_st * kScaleStage;
     uint8_t* nxt = lds + nxt_st * kStage;
-    const int k_nxt = (kt + kStages - 1) * kBK;
-    const int k_b2 = (kt + 2 < KT ? kt + 2 : KT - 1) * kBK;  // two-stage B tile
+    const int k_nxt = kb(kt + kStages - 1) * kBK;
+    const int k_b2 = kb(kt + 2 < KT ? kt + 2 : KT - 1) * kBK;  // two-stage B tile
     // this wave's loads of stage kt have landed: only those of later stages
     // may still be in flight (two stages: stage kt+1's B tile, issued last)
     if constexpr (kSplitB) {
@@ -517,7 +528,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
     auto issue_slot = [&](auto sc, auto kb_c) {  // slot S; kb_c: B tile two stages ahead
       constexpr int S = decltype(sc)::value;
       if constexpr (S < kS0)
-        load_scales(kt + kStages - 1, nxt_st);
+        load_scales(kb(kt + kStages - 1), nxt_st);
       else if constexpr (S - kS0 < kPerA)
         ldA.template load_group<(S - kS0 < kPerA ? S - kS0 : 0)>(k_nxt, nxt, wave);
       else if constexpr (decltype(kb_c)::value)
@@ -753,6 +764,37 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
 
   all_steps();
 
+  if constexpr (KS > 1) {
+    // the groups' partial tiles: group k > 0 writes its accumulators to LDS
+    // (the operand stages are free once every load has landed and every
+    // wave is past its last step), group 0 adds them in group order
+    float* const red = reinterpret_cast<float*>(lds_all);
+    static_assert((KS - 1) * kWaves * TI * TJ * 4 * 64 * 4 <= KS * kGroupBytes, "partials fit the stages");
+    wait_vmem_all();
+    __syncthreads();
+    if (kg > 0) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            red[(((kg - 1) * kWaves + wave) * (TI * TJ * 4) + (i * TJ + j) * 4 + r) * 64 + lane] = acc[i][j][r];
+    }
+    __syncthreads();
+    if (kg == 0) {
+#pragma unroll
+      for (int k = 1; k < KS; ++k)
+#pragma unroll
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              acc[i][j][r] += red[(((k - 1) * kWaves + wave) * (TI * TJ * 4) + (i * TJ + j) * 4 + r) * 64 + lane];
+    }
+  }
+
   // Epilogue: whole-K scales for tensor / row pairs, bf16 RNE, then the
   // tile goes through LDS (the operand stages are free now) so that global
   // stores are whole 16-byte chunks of contiguous C rows.  LDS row m of the
@@ -782,27 +824,29 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
     }
   }
   wait_vmem_all();  // no load may still be writing LDS
-  __syncthreads();  // every wave is done with the operand stages
+  __syncthreads();  // every wave is done with the operand stages (and the partials)
   constexpr int kRowBytes = BN * 2;
   constexpr int kChunkMask = kRowBytes / 16 < 16 ? kRowBytes / 16 - 1 : 15;  // the swizzle stays in the row
+  if (kg == 0) {
 #pragma unroll
-  for (int i = 0; i < TI; ++i) {
-    const int mt = wm + i * 16 + (lane & 15);  // row within the tile
+    for (int i = 0; i < TI; ++i) {
+      const int mt = wm + i * 16 + (lane & 15);  // row within the tile
 #pragma unroll
-    for (int j = 0; j < TJ; ++j) {
-      const int nt = wn + j * 16 + (lane >> 4) * 4;  // column within the tile
-      const int chunk = (nt * 2) >> 4, half = ((nt * 2) >> 3) & 1;
-      *reinterpret_cast<uint2*>(lds + mt * kRowBytes + ((chunk ^ (mt & kChunkMask)) << 4) + half * 8) =
-          packed[i][j];
+      for (int j = 0; j < TJ; ++j) {
+        const int nt = wn + j * 16 + (lane >> 4) * 4;  // column within the tile
+        const int chunk = (nt * 2) >> 4, half = ((nt * 2) >> 3) & 1;
+        *reinterpret_cast<uint2*>(lds_all + mt * kRowBytes + ((chunk ^ (mt & kChunkMask)) << 4) + half * 8) =
+            packed[i][j];
+      }
     }
   }
   __syncthreads();
   constexpr int kChunksPerRow = kRowBytes / 16;
-  constexpr int kThreads = kWaves * 64;
+  constexpr int kThreads = KS * kWaves * 64;
   constexpr int kRowsPerPass = kThreads / kChunksPerRow;
   if constexpr (QOUT) {
     static_assert(kChunksPerRow % 16 == 0, "a 128-column unit per DPP row");
-    store_quantized<BM / kRowsPerPass, kRowBytes, kChunkMask, kRowsPerPass>(g, lds, m0, n0, kChunksPerRow);
+    store_quantized<BM / kRowsPerPass, kRowBytes, kChunkMask, kRowsPerPass>(g, lds_all, m0, n0, kChunksPerRow);
     return;
   }
   const int c = threadIdx.x % kChunksPerRow;
@@ -811,7 +855,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   for (int mt = threadIdx.x / kChunksPerRow; mt < BM; mt += kRowsPerPass) {
     const int64_t m = m0 + mt;
     if (m >= g.M || n >= g.N) continue;
-    const uint4 v = *reinterpret_cast<const uint4*>(lds + mt * kRowBytes + ((c ^ (mt & kChunkMask)) << 4));
+    const uint4 v = *reinterpret_cast<const uint4*>(lds_all + mt * kRowBytes + ((c ^ (mt & kChunkMask)) << 4));
     uint16_t* dst = g.C + m * g.ldc + n;
     if (n + 8 <= g.N) {
       // non-temporal: C is not read again here, and streaming it out keeps
@@ -832,11 +876,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   }
 }
 
-template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT, int KS = 1>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64 * KS) void gemm_kernel(GemmArgs g) {
   int tm, tn;
   tile_coords<BM, BN>(g.M, g.N, blockIdx.x, tm, tn);
-  gemm_tile<PAIR, BM, BN, WM, WN, QOUT, FMT>(g, tm, tn);
+  gemm_tile<PAIR, BM, BN, WM, WN, QOUT, FMT, KS>(g, tm, tn);
 }
 
 // Grouped GEMM: one launch over several problems that share the pair, the
@@ -844,23 +888,32 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 // operand, several weights and outputs).  The workgroups' XCD-ordered
 // positions run over the problems' rasters one after another; the problem
 // of a position is found from the prefix sums of the tile counts.
-template <int PAIR, int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_grouped_kernel(GemmGroup gs) {
+template <int PAIR, int BM, int BN, int WM, int WN, int KS = 1>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64 * KS) void gemm_grouped_kernel(GemmGroup gs) {
   const int id = xcd_order(gs.tile_start[gs.count], blockIdx.x);
   int p = 0;
   for (int i = 1; i < gs.count; ++i) p += id >= gs.tile_start[i] ? 1 : 0;
   int tm, tn;
   raster<BM, BN>(gs.prob[p].M, gs.prob[p].N, id - gs.tile_start[p], tm, tn);
-  gemm_tile<PAIR, BM, BN, WM, WN, false, 0>(gs.prob[p], tm, tn);
+  gemm_tile<PAIR, BM, BN, WM, WN, false, 0, KS>(gs.prob[p], tm, tn);
 }
 
-template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT>
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT, int KS = 1>
 hipError_t launch_tiles(const GemmArgs& g, hipStream_t s) {
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   if (tiles <= 0 || tiles > 0x7fffffff) return hipErrorInvalidValue;
-  constexpr int threads = (BM / WM) * (BN / WN) * 64;
-  gemm_kernel<PAIR, BM, BN, WM, WN, QOUT, FMT><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
+  constexpr int threads = (BM / WM) * (BN / WN) * 64 * KS;
+  gemm_kernel<PAIR, BM, BN, WM, WN, QOUT, FMT, KS><<<dim3((unsigned)tiles), threads, 0, s>>>(g);
   return hipGetLastError();
+}
+
+// Two K groups per 64 x 64 tile (one workgroup of 8 waves per CU) when there
+// are at most 256 such tiles, so that a CU would hold one workgroup anyway,
+// and the K blocks split evenly; more tiles keep two 4-wave workgroups per
+// CU (measured: 256 x 12288 x 4096 35 -> 28 us with groups, 256 x 4096 x
+// 12288 with its 768 tiles 31 -> 34 us).
+inline bool k_groups(const GemmArgs& g) {
+  return ((g.M + 63) / 64) * ((g.N + 63) / 64) <= 256 && (g.K / kBK) % 2 == 0;
 }
 
 // 256 x 256 tiles (8 waves of 128 x 64) when they fill the chip at least
@@ -879,6 +932,7 @@ hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
     return launch_tiles<PAIR, 128, 128, 64, 64, QOUT, FMT>(g, s);
   } else {
     if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64, QOUT, FMT>(g, s);
+    if (k_groups(g)) return launch_tiles<PAIR, 64, 64, 32, 32, QOUT, FMT, 2>(g, s);
     return launch_tiles<PAIR, 64, 64, 32, 32, QOUT, FMT>(g, s);
   }
 }
@@ -961,18 +1015,32 @@ FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 64, 64, 32, 32)
 #undef FP8Q_GEMM_KERNEL
 #undef FP8Q_GEMM_KERNEL_FMT
+#define FP8Q_GEMM_KERNEL_KS2(PAIR, FMT) template __global__ void gemm_kernel<PAIR, 64, 64, 32, 32, false, FMT, 2>(GemmArgs);
+FP8Q_GEMM_KERNEL_KS2(kPairTensor, 0)
+FP8Q_GEMM_KERNEL_KS2(kPairRow, 0)
+FP8Q_GEMM_KERNEL_KS2(kPairBlockE8, 0)
+FP8Q_GEMM_KERNEL_KS2(kPairBlock, 0)
+FP8Q_GEMM_KERNEL_KS2(kPairBlock, 1)
+FP8Q_GEMM_KERNEL_KS2(kPairBlock, 2)
+FP8Q_GEMM_KERNEL_KS2(kPairBlock, 3)
+FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 0)
+FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 1)
+FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 2)
+FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 3)
+#undef FP8Q_GEMM_KERNEL_KS2
 template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true, 0>(GemmArgs);
 template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true, 0>(GemmArgs);
-#define FP8Q_GEMM_GROUPED(PAIR)                                                  \
-  template __global__ void gemm_grouped_kernel<PAIR, 256, 256, 128, 64>(GemmGroup); \
-  template __global__ void gemm_grouped_kernel<PAIR, 128, 128, 64, 64>(GemmGroup);  \
-  template __global__ void gemm_grouped_kernel<PAIR, 64, 64, 32, 32>(GemmGroup);
+#define FP8Q_GEMM_GROUPED(PAIR)                                                     \
+  template __global__ void gemm_grouped_kernel<PAIR, 256, 256, 128, 64>(GemmGroup);    \
+  template __global__ void gemm_grouped_kernel<PAIR, 128, 128, 64, 64>(GemmGroup);     \
+  template __global__ void gemm_grouped_kernel<PAIR, 64, 64, 32, 32>(GemmGroup);       \
+  template __global__ void gemm_grouped_kernel<PAIR, 64, 64, 32, 32, 2>(GemmGroup);
 FP8Q_GEMM_GROUPED(kPairTensor)
 FP8Q_GEMM_GROUPED(kPairRow)
 FP8Q_GEMM_GROUPED(kPairBlock)
 #undef FP8Q_GEMM_GROUPED
 
-template <int PAIR, int BM, int BN, int WM, int WN>
+template <int PAIR, int BM, int BN, int WM, int WN, int KS = 1>
 hipError_t launch_grouped_tiles(GemmGroup gs, hipStream_t s) {
   int64_t total = 0;
   for (int i = 0; i < gs.count; ++i) {
@@ -982,23 +1050,42 @@ hipError_t launch_grouped_tiles(GemmGroup gs, hipStream_t s) {
   }
   gs.tile_start[gs.count] = (int)total;
   if (total <= 0) return hipErrorInvalidValue;
-  constexpr int threads = (BM / WM) * (BN / WN) * 64;
-  gemm_grouped_kernel<PAIR, BM, BN, WM, WN><<<dim3((unsigned)total), threads, 0, s>>>(gs);
+  constexpr int threads = (BM / WM) * (BN / WN) * 64 * KS;
+  gemm_grouped_kernel<PAIR, BM, BN, WM, WN, KS><<<dim3((unsigned)total), threads, 0, s>>>(gs);
   return hipGetLastError();
 }
 
-// The tile size from the tile counts over all problems, as launch_pair
-// chooses it for one.
+// Each problem goes to the kernel a single call would give it.  The tiled
+// kernels without K groups all sum K in one order, so one launch takes every
+// problem a single call would give one of them (the tile size from their
+// tile count over all, as launch_pair chooses it for one: for a skinny
+// problem among large ones that is a larger tile than its own, with the same
+// bits); the problems a single call would split into K groups (another
+// order of the K sum) go to a second launch.
 template <int PAIR>
 hipError_t launch_grouped_pair(const GemmGroup& gs, hipStream_t s) {
+  GemmGroup tiled{}, thin{};
   int64_t big = 0, mid = 0;
   for (int i = 0; i < gs.count; ++i) {
-    big += ((gs.prob[i].M + 255) / 256) * ((gs.prob[i].N + 255) / 256);
-    mid += ((gs.prob[i].M + 127) / 128) * ((gs.prob[i].N + 127) / 128);
+    const GemmArgs& g = gs.prob[i];
+    const int64_t big_i = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+    const int64_t mid_i = ((g.M + 127) / 128) * ((g.N + 127) / 128);
+    if (big_i < 512 && mid_i < 256 && k_groups(g)) {
+      thin.prob[thin.count++] = g;
+    } else {
+      tiled.prob[tiled.count++] = g;
+      big += big_i;
+      mid += mid_i;
+    }
   }
-  if (big >= 512) return launch_grouped_tiles<PAIR, 256, 256, 128, 64>(gs, s);
-  if (mid >= 256) return launch_grouped_tiles<PAIR, 128, 128, 64, 64>(gs, s);
-  return launch_grouped_tiles<PAIR, 64, 64, 32, 32>(gs, s);
+  if (tiled.count) {
+    const hipError_t e = big >= 512   ? launch_grouped_tiles<PAIR, 256, 256, 128, 64>(tiled, s)
+                         : mid >= 256 ? launch_grouped_tiles<PAIR, 128, 128, 64, 64>(tiled, s)
+                                      : launch_grouped_tiles<PAIR, 64, 64, 32, 32>(tiled, s);
+    if (e != hipSuccess) return e;
+  }
+  if (thin.count) return launch_grouped_tiles<PAIR, 64, 64, 32, 32, 2>(thin, s);
+  return hipSuccess;
 }
 
 }  // namespace gemm_detail

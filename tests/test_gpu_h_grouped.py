@@ -57,6 +57,18 @@ def test_qkv_shared_input_small(ga, gb):
     check_group([x, x, x], ws, ga, gb, label="qkv small")
 
 
+def test_mixed_tiled_and_k_group_problems():
+    """A large problem (128 x 128 or larger tiles) and a skinny one that a
+    single call splits into two K groups: the grouped call runs them in two
+    launches, each output still fp8q_gemm's bit for bit."""
+    x1 = synth.activations(4096, 512, seed=211, outlier_seed=212, device=DEV)
+    x2 = synth.activations(192, 512, seed=213, outlier_seed=214, device=DEV)
+    w1 = synth.weights(2048, 512, seed=215, device=DEV)
+    w2 = synth.weights(384, 512, seed=216, device=DEV)
+    check_group([x1, x2], [w1, w2], fp8q.BLOCK_1x128, fp8q.BLOCK_128x128, rows=_par.sample_rows(192),
+                label="mixed tiled and K groups")
+
+
 def test_distinct_inputs_and_sizes():
     """Problems with their own inputs, token counts and widths (every tile
     size of one launch is the same; the problems' rasters follow each other)."""
