@@ -96,6 +96,19 @@ def test_small_all_pairs(pair):
     run_pair(a, b, ga, gb, label=pair)
 
 
+@pytest.mark.parametrize("pair", list(PAIRS))
+def test_small_all_pairs_k_groups(pair):
+    """Eight K blocks on few 64 x 64 tiles: the kernel splits the K blocks
+    over two groups of waves and sums their partial tiles (ragged M and,
+    where the pair allows it, ragged N)."""
+    ga, gb = PAIRS[pair]
+    M, K = 200, 1024
+    N = 384 if gb == fp8q.BLOCK_128x128 else 392
+    a = synth.activations(M, K, seed=161, outlier_seed=162, device=DEV)
+    b = synth.weights(N, K, seed=163, device=DEV)
+    run_pair(a, b, ga, gb, label=pair + " K groups")
+
+
 @pytest.mark.parametrize("pair", ["tensor", "row"])
 @pytest.mark.parametrize("M,K,N", [(200, 256, 390), (16384 + 96, 128, 8192 + 6)])
 def test_ragged_columns_padded_output(pair, M, K, N):
