@@ -85,6 +85,10 @@ def test_quantize_rejections(L):
     assert quant(L, rows=200, g=4) == -2                     # 128x1 needs rows % 128
     assert quant(L, rows=200, g=5) == -2
     assert quant(L, rows=200, g=1, flags=1, ldc=208) == -2   # transposed: rows % 16
+    assert quant(L, rows=65535 * 32 + 32, g=3) == -2          # grid limit of the 32-row tiles
+    assert quant(L, rows=65535 * 32 + 32, g=0) == -2
+    assert quant(L, rows=65535 * 128 + 128, g=5) == -2       # grid limit of the 128-row tiles
+    assert quant(L, rows=65535 * 128 + 128, g=1, flags=1, ldc=65535 * 128 + 128) == -2
     assert quant(L, x=FAKE + 2) == -3
     assert quant(L, codes=FAKE + 8) == -3
     assert quant(L, scales=FAKE + 2) == -3
