@@ -106,8 +106,7 @@ int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g,
  *   scales  fp32, fp8q_scales_count(rows, cols, g, flags) entries
  * Shape rules: cols % 16 == 0, and rows % 16 == 0 when transposed; a
  * dimension a 128-block splits (cols for 1x128 and 128x128, rows for 128x1
- * and 128x128) must be a multiple of 128; rows <= 65535 x 32 for 1x128 and
- * TENSOR without FP8Q_OUT_TRANSPOSED, else rows <= 65535 x 128 (else
+ * and 128x128) must be a multiple of 128; rows <= 65535 x 128 (else
  * FP8Q_ERR_UNSUPPORTED).  x must not overlap codes or scales.
  * Alignment: x and codes 16-byte aligned, ldx % 8 == 0, ldc % 16 == 0,
  * scales 4-byte aligned (else FP8Q_ERR_ALIGN).

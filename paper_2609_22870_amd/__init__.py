@@ -135,6 +135,45 @@ def _ld(t):
     return t.stride(0)
 
 
+def _matrix(t, dtype, what, shape=None, device=None):
+    """t as a row-major 2-D CUDA tensor of dtype (and of shape / on device
+    when given): the kernels read and write exactly that region, so a
+    tensor of another shape would be read or written past its end."""
+    if not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda or t.dim() != 2:
+        raise ValueError("%s must be a 2-D %s CUDA tensor" % (what, dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, not %s" % (what, tuple(shape), tuple(t.shape)))
+    if device is not None and t.device != device:
+        raise ValueError("%s must be on %s" % (what, device))
+    _ld(t)
+    return t
+
+
+def _vector(t, dtype, n, what, device):
+    """t as a contiguous CUDA tensor of dtype with at least n elements."""
+    if (not isinstance(t, torch.Tensor) or t.dtype != dtype or not t.is_cuda or not t.is_contiguous()
+            or t.device != device):
+        raise ValueError("%s must be a contiguous %s tensor on %s" % (what, dtype, device))
+    if t.numel() < n:
+        raise ValueError("%s holds %d elements, %d needed" % (what, t.numel(), n))
+    return t
+
+
+def _operands(a, sa, ga, b, sb, gb):
+    """The checks shared by the GEMM entry points: FP8 codes a [M, K] and b
+    [N, K] on one device, and scale arrays holding at least the counts
+    their granularities give for those shapes; returns M, N, K."""
+    _matrix(a, torch.uint8, "a")
+    _matrix(b, torch.uint8, "b", device=a.device)
+    M, K = a.shape
+    N, K2 = b.shape
+    if K != K2:
+        raise ValueError("contraction sizes differ")
+    _vector(sa, torch.float32, max(scales_count(M, K, ga), 0), "sa", a.device)
+    _vector(sb, torch.float32, max(scales_count(N, K, gb), 0), "sb", a.device)
+    return M, N, K
+
+
 def scales_count(rows, cols, granularity, transposed=False):
     n = lib().fp8q_scales_count(rows, cols, granularity, OUT_TRANSPOSED if transposed else 0)
     if n < 0:
@@ -150,15 +189,16 @@ def quantize(x, granularity, transposed=False, codes=None, scales=None, pow2=Fal
     include/fp8q.h.  pow2: power-of-two scales (FP8Q_POW2_SCALE); e5m2:
     E5M2 codes (FP8Q_E5M2).
     """
-    if x.dtype != torch.bfloat16 or not x.is_cuda:
-        raise ValueError("x must be a bf16 CUDA tensor")
+    _matrix(x, torch.bfloat16, "x")
     rows, cols = x.shape
     oshape = (cols, rows) if transposed else (rows, cols)
+    n = scales_count(rows, cols, granularity, transposed)
     if codes is None:
         codes = torch.empty(oshape, dtype=torch.uint8, device=x.device)
+    _matrix(codes, torch.uint8, "codes", oshape, x.device)
     if scales is None:
-        scales = torch.empty(scales_count(rows, cols, granularity, transposed),
-                             dtype=torch.float32, device=x.device)
+        scales = torch.empty(n, dtype=torch.float32, device=x.device)
+    _vector(scales, torch.float32, n, "scales", x.device)
     st = lib().fp8q_quantize(x.data_ptr(), rows, cols, _ld(x), granularity,
                              (OUT_TRANSPOSED if transposed else 0) | (POW2_SCALE if pow2 else 0)
                              | (E5M2 if e5m2 else 0),
@@ -173,19 +213,21 @@ def quantize_dual(x, codes_r=None, scales_r=None, codes_t=None, scales_t=None, p
     one read: (codes_r, scales_r) = quantize(x, BLOCK_1x128) and
     (codes_t, scales_t) = quantize(x, BLOCK_128x1, transposed=True), with
     the same pow2 / e5m2 options."""
-    if x.dtype != torch.bfloat16 or not x.is_cuda:
-        raise ValueError("x must be a bf16 CUDA tensor")
+    _matrix(x, torch.bfloat16, "x")
     rows, cols = x.shape
+    nr, nt = scales_count(rows, cols, BLOCK_1x128), scales_count(rows, cols, BLOCK_128x1, True)
     if codes_r is None:
         codes_r = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
     if scales_r is None:
-        scales_r = torch.empty(scales_count(rows, cols, BLOCK_1x128),
-                               dtype=torch.float32, device=x.device)
+        scales_r = torch.empty(nr, dtype=torch.float32, device=x.device)
     if codes_t is None:
         codes_t = torch.empty((cols, rows), dtype=torch.uint8, device=x.device)
     if scales_t is None:
-        scales_t = torch.empty(scales_count(rows, cols, BLOCK_128x1, True),
-                               dtype=torch.float32, device=x.device)
+        scales_t = torch.empty(nt, dtype=torch.float32, device=x.device)
+    _matrix(codes_r, torch.uint8, "codes_r", (rows, cols), x.device)
+    _matrix(codes_t, torch.uint8, "codes_t", (cols, rows), x.device)
+    _vector(scales_r, torch.float32, nr, "scales_r", x.device)
+    _vector(scales_t, torch.float32, nt, "scales_t", x.device)
     st = lib().fp8q_quantize_dual(x.data_ptr(), rows, cols, _ld(x),
                                   (POW2_SCALE if pow2 else 0) | (E5M2 if e5m2 else 0),
                                   codes_r.data_ptr(), _ld(codes_r),
@@ -201,12 +243,10 @@ def gemm(a, sa, ga, b, sb, gb, out=None):
     a, b: uint8 E4M3 codes, K contiguous; sa, sb: fp32 scales for the
     granularities ga, gb (pairs listed in include/fp8q.h).
     """
-    M, K = a.shape
-    N, K2 = b.shape
-    if K != K2:
-        raise ValueError("contraction sizes differ")
+    M, N, K = _operands(a, sa, ga, b, sb, gb)
     if out is None:
         out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    _matrix(out, torch.bfloat16, "out", (M, N), a.device)
     st = lib().fp8q_gemm(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
                          b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                          out.data_ptr(), _ld(out), _stream(a))
@@ -223,13 +263,19 @@ def gemm_grouped(problems, ga, gb, outs=None):
     if not 1 <= len(problems) <= MAX_GROUP:
         raise ValueError("1 .. %d problems" % MAX_GROUP)
     K = problems[0][0].shape[1]
+    dev = problems[0][0].device
+    for a, sa, b, sb in problems:
+        _operands(a, sa, ga, b, sb, gb)
+        if a.shape[1] != K or a.device != dev:
+            raise ValueError("every problem must have the same K and device")
     if outs is None:
         outs = [torch.empty((a.shape[0], b.shape[0]), dtype=torch.bfloat16, device=a.device)
                 for a, _, b, _ in problems]
+    if len(outs) != len(problems):
+        raise ValueError("one output per problem")
     arr = (GemmProblem * len(problems))()
     for i, ((a, sa, b, sb), c) in enumerate(zip(problems, outs)):
-        if a.shape[1] != K or b.shape[1] != K:
-            raise ValueError("every problem must have the same K")
+        _matrix(c, torch.bfloat16, "outs[%d]" % i, (a.shape[0], b.shape[0]), dev)
         arr[i] = GemmProblem(a.data_ptr(), sa.data_ptr(), _ld(a), b.data_ptr(), sb.data_ptr(), _ld(b),
                              c.data_ptr(), _ld(c), a.shape[0], b.shape[0])
     st = lib().fp8q_gemm_grouped(arr, len(problems), ga, gb, K, _stream(problems[0][0]))
@@ -240,12 +286,10 @@ def gemm_grouped(problems, ga, gb, outs=None):
 def gemm_formats(a, sa, ga, b, sb, gb, formats, out=None):
     """gemm() with E5M2 codes for A (formats & A_E5M2) and/or B (formats &
     B_E5M2): the backward pairs (1x128, 128x128) and (1x128, 1x128)."""
-    M, K = a.shape
-    N, K2 = b.shape
-    if K != K2:
-        raise ValueError("contraction sizes differ")
+    M, N, K = _operands(a, sa, ga, b, sb, gb)
     if out is None:
         out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    _matrix(out, torch.bfloat16, "out", (M, N), a.device)
     st = lib().fp8q_gemm_formats(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
                                  b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                                  formats, out.data_ptr(), _ld(out), _stream(a))
@@ -256,12 +300,10 @@ def gemm_formats(a, sa, ga, b, sb, gb, formats, out=None):
 def gemm_pow2(a, sa, ga, b, sb, gb, out=None):
     """gemm() for operands quantized with power-of-two scales (pow2=True):
     the block scales enter the matrix instruction as exponents."""
-    M, K = a.shape
-    N, K2 = b.shape
-    if K != K2:
-        raise ValueError("contraction sizes differ")
+    M, N, K = _operands(a, sa, ga, b, sb, gb)
     if out is None:
         out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    _matrix(out, torch.bfloat16, "out", (M, N), a.device)
     st = lib().fp8q_gemm_pow2(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
                               b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                               out.data_ptr(), _ld(out), _stream(a))
@@ -274,15 +316,14 @@ def gemm_quantized(a, sa, ga, b, sb, gb, codes=None, scales=None):
     (the next layer's activation operand), in one kernel.  Returns (codes
     uint8 [M, N], scales fp32 in the 1x128 layout), exactly
     quantize(gemm(a, sa, ga, b, sb, gb), BLOCK_1x128)."""
-    M, K = a.shape
-    N, K2 = b.shape
-    if K != K2:
-        raise ValueError("contraction sizes differ")
+    M, N, K = _operands(a, sa, ga, b, sb, gb)
+    n = scales_count(M, N, BLOCK_1x128)
     if codes is None:
         codes = torch.empty((M, N), dtype=torch.uint8, device=a.device)
     if scales is None:
-        scales = torch.empty(scales_count(M, N, BLOCK_1x128), dtype=torch.float32,
-                             device=a.device)
+        scales = torch.empty(n, dtype=torch.float32, device=a.device)
+    _matrix(codes, torch.uint8, "codes", (M, N), a.device)
+    _vector(scales, torch.float32, n, "scales", a.device)
     st = lib().fp8q_gemm_quantized(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
                                    b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                                    codes.data_ptr(), _ld(codes), scales.data_ptr(),
@@ -312,6 +353,8 @@ def calibrate_clip(adv, w_tis, pi_sampler, r_bf16, r_fp8, l_old, h_old, config=N
         workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=adv.device)
     if result is None:
         result = torch.empty(ctypes.sizeof(ClipResult), dtype=torch.uint8, device=adv.device)
+    _vector(workspace, torch.uint8, need, "workspace", adv.device)
+    _vector(result, torch.uint8, ctypes.sizeof(ClipResult), "result", adv.device)
     st = lib().fp8q_calibrate_clip(*(t.data_ptr() for t in ts), n, float(l_old), float(h_old),
                                    ctypes.byref(cfg), workspace.data_ptr(), workspace.numel(),
                                    result.data_ptr(), _stream(adv))
@@ -329,6 +372,7 @@ def cast_f32(x, scale, codes=None, e5m2=False):
         raise ValueError("x must be a contiguous fp32 CUDA tensor")
     if codes is None:
         codes = torch.empty(x.shape, dtype=torch.uint8, device=x.device)
+    _vector(codes, torch.uint8, x.numel(), "codes", x.device)
     fn = lib().fp8q_cast_f32_e5m2 if e5m2 else lib().fp8q_cast_f32
     st = fn(x.data_ptr(), x.numel(), float(scale), codes.data_ptr(), _stream(x))
     _check(st, "fp8q_cast_f32_e5m2" if e5m2 else "fp8q_cast_f32")

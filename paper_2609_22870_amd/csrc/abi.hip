@@ -139,10 +139,7 @@ fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx
   const bool splits_rows = g == FP8Q_BLOCK_128x1 || g == FP8Q_BLOCK_128x128;
   if (cols % 16 || (t && rows % 16)) return FP8Q_ERR_UNSUPPORTED;
   if ((splits_cols && cols % 128) || (splits_rows && rows % 128)) return FP8Q_ERR_UNSUPPORTED;
-  // grid.y limit: tiles of 32 rows for 1x128 and TENSOR without
-  // transposition, of 128 rows for the tile kernels of the others
-  const int64_t tile_rows = (!t && (g == FP8Q_BLOCK_1x128 || g == FP8Q_TENSOR)) ? 32 : 128;
-  if (rows > (int64_t)65535 * tile_rows) return FP8Q_ERR_UNSUPPORTED;
+  if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || ldx % 8 || ldc % 16)
     return FP8Q_ERR_ALIGN;
   fp8q::QuantArgs a;

@@ -85,10 +85,8 @@ def test_quantize_rejections(L):
     assert quant(L, rows=200, g=4) == -2                     # 128x1 needs rows % 128
     assert quant(L, rows=200, g=5) == -2
     assert quant(L, rows=200, g=1, flags=1, ldc=208) == -2   # transposed: rows % 16
-    assert quant(L, rows=65535 * 32 + 32, g=3) == -2          # grid limit of the 32-row tiles
-    assert quant(L, rows=65535 * 32 + 32, g=0) == -2
-    assert quant(L, rows=65535 * 128 + 128, g=5) == -2       # grid limit of the 128-row tiles
-    assert quant(L, rows=65535 * 128 + 128, g=1, flags=1, ldc=65535 * 128 + 128) == -2
+    assert quant(L, rows=65535 * 128 + 128, g=5) == -2       # row limit
+    assert quant(L, rows=65535 * 128 + 128, g=3) == -2
     assert quant(L, x=FAKE + 2) == -3
     assert quant(L, codes=FAKE + 8) == -3
     assert quant(L, scales=FAKE + 2) == -3
@@ -277,3 +275,21 @@ def test_calibrate_clip_workspace_and_rejections(L):
     assert calib(L, ptrs=(FAKE + 4,) + (FAKE,) * 4) == -3
     assert calib(L, ws=FAKE + 4) == -3
     assert calib(L, res=FAKE + 4) == -3
+
+
+def test_binding_rejects_short_or_misshapen_buffers():
+    """The Python binding checks caller-supplied outputs and scale arrays
+    before any call: the kernels read and write exactly the sizes the shapes
+    give, so a smaller tensor would be read or written past its end.  (CPU
+    tensors fail the same checks; no kernel runs.)"""
+    import torch
+    import paper_2609_22870_amd as fp8q
+    x = torch.zeros((256, 256), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        fp8q.quantize(x, fp8q.BLOCK_1x128)                      # not a CUDA tensor
+    a = torch.zeros((256, 256), dtype=torch.uint8)
+    s = torch.zeros(512, dtype=torch.float32)
+    with pytest.raises(ValueError):
+        fp8q.gemm(a, s, fp8q.BLOCK_1x128, a, s, fp8q.BLOCK_128x128)
+    with pytest.raises(ValueError):
+        fp8q.cast_f32(torch.zeros(16), 1.0)

@@ -226,3 +226,23 @@ def test_full_32b_backward_operands():
     del dy
     x = synth.activations(16384, 5120, seed=synth.seed_for(5, 0), outlier_seed=synth.seed_for(5, 3), device=DEV)
     check(x.cpu(), fp8q.BLOCK_128x1, transposed=True, label="X^T 32B")
+
+
+def test_binding_checks_buffers():
+    """Caller-supplied outputs and scale arrays of the wrong shape or too
+    few elements are refused by the binding before any kernel runs."""
+    x = synth.activations(256, 256, seed=1, outlier_seed=2).to(DEV)
+    with pytest.raises(ValueError):
+        fp8q.quantize(x, fp8q.BLOCK_1x128, scales=torch.empty(10, dtype=torch.float32, device=DEV))
+    with pytest.raises(ValueError):
+        fp8q.quantize(x, fp8q.BLOCK_1x128, codes=torch.empty((256, 128), dtype=torch.uint8, device=DEV))
+    A, sA = fp8q.quantize(x, fp8q.BLOCK_1x128)
+    B, sB = fp8q.quantize(x, fp8q.BLOCK_128x128)
+    with pytest.raises(ValueError):
+        fp8q.gemm(A, sA[:10], fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128)
+    with pytest.raises(ValueError):
+        fp8q.gemm(A, sA, fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128,
+                  out=torch.empty((256, 128), dtype=torch.bfloat16, device=DEV))
+    with pytest.raises(ValueError):
+        fp8q.gemm_quantized(A, sA, fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128,
+                            scales=torch.empty(3, dtype=torch.float32, device=DEV))
