@@ -13,12 +13,13 @@
 //     H_k the numerator sum with r_FP8 < H_k.
 // A token's grid position is found once (an estimate from its ratio,
 // corrected by exact comparisons with the float64 grid points) and the
-// token is added to that bin of its thread's own column of LDS bins; the
-// threshold sums of every grid point are prefix sums over the bins.  Sums
-// are float64 in a fixed order (per thread in token order, the threads of a
-// block in order, the blocks by a fixed lane-then-tree order, the bins in
-// order), so the result is the same on every run.  A second kernel reduces
-// the blocks and runs the searches and SmoothUpdate.
+// token is added to that bin of its wave's bins, held in registers (bin r
+// in lane r); the threshold sums of every grid point are prefix sums over
+// the bins.  Sums are float64 in a fixed order (per thread in token order,
+// or per wave in token-group then lane order for the bins, the threads or
+// waves of a block in order, the blocks by a fixed lane-then-tree order,
+// the bins in order), so the result is the same on every run.  A second
+// kernel reduces the blocks and runs the searches and SmoothUpdate.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -85,44 +86,52 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
-// Per-thread bins in LDS, one column per thread: row q of thread t at
-// element q * (T + 1) + t (the odd row length keeps both the per-token
-// updates, where lanes hit different rows, and the end-of-block row sums,
-// where lanes walk different rows in step, spread over the banks).  Rows
-// of `val`: the lower bins' Eq. 5 denominator sums (negative tokens), then
-// the upper bins' numerator sums (positive tokens); rows of `cnt`: the
-// lower bins' counts.
-template <int KL, int KH, int T>
-struct Bins {
-  static constexpr int kRow = T + 1;
-  static constexpr int kNum0 = KL + 1;
-  double val[(KL + KH + 2) * kRow];
-  int cnt[(KL + 1) * kRow];
+// Bins of a wave, in registers: val bin r (the lower bins' Eq. 5 denominator
+// sums, r = j <= KL, then the upper bins' numerator sums, r = KL + 1 + j) in
+// lane r of `lo` (r < 64) or lane r - 64 of `hi`; the lower bins' counts in
+// lane j of `cnt`.  A token that falls in one of them (a ratio inside a
+// search interval: about one token in a hundred) is added by the bin's
+// lane, the wave's binned tokens one after another in lane order, so every
+// bin sums in a fixed order and no LDS is needed: the kernel runs three
+// waves per SIMD instead of the one that per-thread LDS bins allowed.
+template <int KL, int KH>
+struct WaveBins {
+  static constexpr int kVal = KL + KH + 2, kNum0 = KL + 1;
+  static_assert(KL + 1 <= 64 && kVal <= 128, "bins fit two lane sets");
+  double lo = 0.0, hi = 0.0;
+  int cnt = 0;
 };
 
 // Per-thread sums in registers.  Most ratios lie between the two search
 // intervals (above the last lower point, below the first upper point), so
 // a negative token usually falls in the top lower bin (nl) and a positive
-// one in the bottom upper bin (0): those two bins are kept here, and only
-// the other tokens go to the LDS bins.  A bin is fed by one of the two
-// only, so every sum still runs in token order.
+// one in the bottom upper bin (0): those two bins are kept here, per
+// thread in token order, and only the other tokens go to the wave's bins.
+// A bin is fed by one of the two only.
 struct Scalars {
   int n_neg, n_pos, cnt_ref, top_cnt;
   double num_ref, den_ref, top_den, bottom_num;
 };
 
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  const uint64_t u = __double_as_longlong(v);
+  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, l), hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), l);
+  return __longlong_as_double(((uint64_t)hi << 32) | lo);
+}
+
 // l_last: the last lower grid point; a negative token above it has every
 // lower point strictly below its ratio (bin nl).  The first upper point is
 // h_min; a positive token below it has no upper point at or below its
 // ratio (bin 0).
-// The token's sums.  NEG / POS: its sign when the whole wave shares it
+// The token's sums (a token with a = 0, also the padding past the end of a
+// range, enters none).  NEG / POS: its sign when the whole wave shares it
 // (the tokens of a response share one advantage, and a wave covers 256
 // consecutive tokens), which drops the other sign's selects; else both are
-// 0 and the token's own sign decides.
-template <int KL, int KH, int T, bool NEG, bool POS>
+// 0 and the token's own sign decides.  Called by every lane of the wave.
+template <int KL, int KH, bool NEG, bool POS>
 __device__ __forceinline__ void add_token(const ClipArgs& p, double l_last, float a, float w, float pi, float rb,
-                                          float rf, Scalars& s, Bins<KL, KH, T>& b) {
-  using B = Bins<KL, KH, T>;
+                                          float rf, Scalars& s, WaveBins<KL, KH>& b) {
+  using B = WaveBins<KL, KH>;
   const double rb64 = rb, rf64 = rf;
   const bool neg = NEG || (!POS && a < 0.0f), pos = POS || (!NEG && a > 0.0f);
   const double wp = (double)w * (double)pi;
@@ -142,13 +151,26 @@ __device__ __forceinline__ void add_token(const ClipArgs& p, double l_last, floa
     bottom = pos && rf64 < p.h_min;
     s.bottom_num += bottom ? tf : 0.0;
   }
-  if ((neg && !top) || (pos && !bottom)) {
-    // lower bins count the grid points strictly below r_FP8; upper bins
-    // the points at or below it
-    const int j = grid_rank(rf64, neg ? p.l_min : p.h_min, p.step, p.inv_step, neg ? p.nl : p.nh, neg);
-    const int t = threadIdx.x;
-    b.val[(neg ? j : B::kNum0 + j) * B::kRow + t] += tf;
-    if (neg) b.cnt[j * B::kRow + t] += 1;
+  const bool binned = (neg && !top) || (pos && !bottom);
+  uint64_t m = __ballot(binned);
+  if (m == 0) return;
+  // lower bins count the grid points strictly below r_FP8; upper bins the
+  // points at or below it
+  const int j = binned ? grid_rank(rf64, neg ? p.l_min : p.h_min, p.step, p.inv_step, neg ? p.nl : p.nh, neg) : 0;
+  const int row = neg ? j : B::kNum0 + j;
+  const int lane = threadIdx.x & 63;
+  while (m) {
+    const int l = __builtin_ctzll(m);
+    m &= m - 1;
+    const int r = __builtin_amdgcn_readlane(row, l);
+    const double v = readlane_f64(tf, l);
+    const bool is_neg = __builtin_amdgcn_readlane(neg ? 1 : 0, l) != 0;
+    if (r < 64) {
+      b.lo += lane == r ? v : 0.0;
+    } else {
+      b.hi += lane == r - 64 ? v : 0.0;
+    }
+    b.cnt += (is_neg && lane == r) ? 1 : 0;
   }
 }
 
@@ -157,8 +179,8 @@ struct Group {
   float4 a, w, pi, rb, rf;
 };
 
-// The group at token i when all four tokens lie before `end` (else zeros:
-// a partial group is read token by token when it is processed).
+// The group at token i; tokens at or past `end` read as a = 0 (they enter
+// no sum).
 __device__ __forceinline__ Group load_group(const ClipArgs& p, int64_t i, int64_t end) {
   Group g;
   if (i + 4 <= end) {
@@ -168,81 +190,99 @@ __device__ __forceinline__ Group load_group(const ClipArgs& p, int64_t i, int64_
     g.rb = *reinterpret_cast<const float4*>(p.rb + i);
     g.rf = *reinterpret_cast<const float4*>(p.rf + i);
   } else {
-    g.a = g.w = g.pi = g.rb = g.rf = make_float4(0.f, 0.f, 0.f, 0.f);
+    float v[5][4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = i + e < end;
+      v[0][e] = ok ? p.adv[i + e] : 0.0f;
+      v[1][e] = ok ? p.w[i + e] : 0.0f;
+      v[2][e] = ok ? p.pi[i + e] : 0.0f;
+      v[3][e] = ok ? p.rb[i + e] : 1.0f;
+      v[4][e] = ok ? p.rf[i + e] : 1.0f;
+    }
+    g.a = make_float4(v[0][0], v[0][1], v[0][2], v[0][3]);
+    g.w = make_float4(v[1][0], v[1][1], v[1][2], v[1][3]);
+    g.pi = make_float4(v[2][0], v[2][1], v[2][2], v[2][3]);
+    g.rb = make_float4(v[3][0], v[3][1], v[3][2], v[3][3]);
+    g.rf = make_float4(v[4][0], v[4][1], v[4][2], v[4][3]);
   }
   return g;
 }
 
-template <int KL, int KH, int T, bool NEG, bool POS>
+template <int KL, int KH, bool NEG, bool POS>
 __device__ __forceinline__ void add_full_group(const ClipArgs& p, double l_last, const Group& g, Scalars& s,
-                                               Bins<KL, KH, T>& b) {
-  add_token<KL, KH, T, NEG, POS>(p, l_last, g.a.x, g.w.x, g.pi.x, g.rb.x, g.rf.x, s, b);
-  add_token<KL, KH, T, NEG, POS>(p, l_last, g.a.y, g.w.y, g.pi.y, g.rb.y, g.rf.y, s, b);
-  add_token<KL, KH, T, NEG, POS>(p, l_last, g.a.z, g.w.z, g.pi.z, g.rb.z, g.rf.z, s, b);
-  add_token<KL, KH, T, NEG, POS>(p, l_last, g.a.w, g.w.w, g.pi.w, g.rb.w, g.rf.w, s, b);
+                                               WaveBins<KL, KH>& b) {
+  add_token<KL, KH, NEG, POS>(p, l_last, g.a.x, g.w.x, g.pi.x, g.rb.x, g.rf.x, s, b);
+  add_token<KL, KH, NEG, POS>(p, l_last, g.a.y, g.w.y, g.pi.y, g.rb.y, g.rf.y, s, b);
+  add_token<KL, KH, NEG, POS>(p, l_last, g.a.z, g.w.z, g.pi.z, g.rb.z, g.rf.z, s, b);
+  add_token<KL, KH, NEG, POS>(p, l_last, g.a.w, g.w.w, g.pi.w, g.rb.w, g.rf.w, s, b);
 }
 
-template <int KL, int KH, int T>
-__device__ __forceinline__ void add_group(const ClipArgs& p, double l_last, const Group& g, int64_t i, int64_t end,
-                                          Scalars& s, Bins<KL, KH, T>& b) {
-  if (i + 4 <= end) {
-    // (a lane past the end of the range votes with the others)
-    const bool all_neg = g.a.x < 0.f && g.a.y < 0.f && g.a.z < 0.f && g.a.w < 0.f;
-    const bool all_pos = g.a.x > 0.f && g.a.y > 0.f && g.a.z > 0.f && g.a.w > 0.f;
-    if (__all(all_neg))
-      add_full_group<KL, KH, T, true, false>(p, l_last, g, s, b);
-    else if (__all(all_pos))
-      add_full_group<KL, KH, T, false, true>(p, l_last, g, s, b);
-    else
-      add_full_group<KL, KH, T, false, false>(p, l_last, g, s, b);
-  } else {
-    for (int64_t q = i; q < end; ++q)
-      add_token<KL, KH, T, false, false>(p, l_last, p.adv[q], p.w[q], p.pi[q], p.rb[q], p.rf[q], s, b);
-  }
+// One group per lane, every lane of the wave (wave-uniform branches only).
+template <int KL, int KH>
+__device__ __forceinline__ void add_group(const ClipArgs& p, double l_last, const Group& g, Scalars& s,
+                                          WaveBins<KL, KH>& b) {
+  const bool all_neg = g.a.x < 0.f && g.a.y < 0.f && g.a.z < 0.f && g.a.w < 0.f;
+  const bool all_pos = g.a.x > 0.f && g.a.y > 0.f && g.a.z > 0.f && g.a.w > 0.f;
+  if (__all(all_neg))
+    add_full_group<KL, KH, true, false>(p, l_last, g, s, b);
+  else if (__all(all_pos))
+    add_full_group<KL, KH, false, true>(p, l_last, g, s, b);
+  else
+    add_full_group<KL, KH, false, false>(p, l_last, g, s, b);
 }
 
 // Partial sums of one block's contiguous token range [b * chunk, ...):
 // thread t takes the 4-token groups t, t + T, ... of the range, in order,
-// with the loads of the next kDepth groups in flight (one wave per SIMD
-// leaves no other wave to hide their latency).
+// with the loads of the next kDepth groups in flight (two: the twelve waves
+// of a block already keep enough loads in flight, and deeper staging cost
+// registers and time, 51.5 against 46.4 us on the paper's batch).  Every
+// lane runs the same number of iterations (groups past the range read as
+// a = 0).
 template <int KL, int KH, int T>
 __global__ __launch_bounds__(T) void clip_stats_kernel(ClipArgs p) {
   using S = Slots<KL, KH>;
-  using B = Bins<KL, KH, T>;
+  using B = WaveBins<KL, KH>;
   constexpr int kWaves = T / 64;
-  __shared__ B bins;
   __shared__ double red[kWaves][5];
-  for (int i = threadIdx.x; i < (KL + KH + 2) * B::kRow; i += T) bins.val[i] = 0.0;
-  for (int i = threadIdx.x; i < (KL + 1) * B::kRow; i += T) bins.cnt[i] = 0;
-  __syncthreads();
+  __shared__ double wval[kWaves][B::kVal];
+  __shared__ int wcnt[kWaves][KL + 1];
   Scalars s{0, 0, 0, 0, 0.0, 0.0, 0.0, 0.0};
+  WaveBins<KL, KH> bins;
   const double l_last = grid_point(p.l_min, p.step, p.nl - 1);
 
-  constexpr int kDepth = 4;
+  constexpr int kDepth = 2;
   constexpr int64_t kStride = 4 * T;
   const int64_t begin = (int64_t)blockIdx.x * p.chunk;
   const int64_t end = begin + p.chunk < p.n ? begin + p.chunk : p.n;
+  const int64_t lane0 = 4 * (int64_t)threadIdx.x;
   Group g[kDepth];
-  int64_t i = begin + 4 * (int64_t)threadIdx.x;
 #pragma unroll
-  for (int d = 0; d < kDepth; ++d) g[d] = load_group(p, i + d * kStride, end);
-  for (; i < end; i += kDepth * kStride) {
+  for (int d = 0; d < kDepth; ++d) g[d] = load_group(p, begin + lane0 + d * kStride, end);
+  for (int64_t base = begin; base < end; base += kDepth * kStride) {
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
-      const int64_t id = i + d * kStride;
-      if (id < end) add_group(p, l_last, g[d], id, end, s, bins);
+      const int64_t id = base + lane0 + d * kStride;
+      if (base + d * kStride < end) add_group(p, l_last, g[d], s, bins);  // (uniform)
       g[d] = load_group(p, id + kDepth * kStride, end);
     }
   }
 
-  // the register-held bins join their LDS rows (which no token touched)
-  bins.val[p.nl * B::kRow + threadIdx.x] = s.top_den;
-  bins.cnt[p.nl * B::kRow + threadIdx.x] = s.top_cnt;
-  bins.val[B::kNum0 * B::kRow + threadIdx.x] = s.bottom_num;
-  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the register-held bins (per thread, token order) join the wave's bins
+  // (no token was added to those two rows there): wave sums
+  const double top_den = wave_sum(s.top_den), bottom_num = wave_sum(s.bottom_num);
+  const double top_cnt = wave_sum((double)s.top_cnt);
+  // the wave's bins to LDS
+  for (int r = lane; r < B::kVal; r += 64) {
+    double v = r < 64 ? bins.lo : bins.hi;
+    if (r == p.nl) v = top_den;
+    if (r == B::kNum0) v = bottom_num;
+    wval[wave][r] = v;
+  }
+  if (lane <= KL) wcnt[wave][lane] = lane == p.nl ? (int)top_cnt : bins.cnt;
 
   // scalars: wave sums, then the waves in order
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const double sv[5] = {(double)s.n_neg, (double)s.n_pos, (double)s.cnt_ref, s.num_ref, s.den_ref};
 #pragma unroll
   for (int q = 0; q < 5; ++q) {
@@ -257,29 +297,42 @@ __global__ __launch_bounds__(T) void clip_stats_kernel(ClipArgs p) {
     for (int q = 1; q < kWaves; ++q) v += red[q][threadIdx.x];
     p.partials[(int64_t)threadIdx.x * p.blocks + out] = v;
   }
-  // bins: thread r sums row r over the threads, in thread order
+  // bins: thread r sums row r over the waves, in wave order
   for (int r = threadIdx.x; r < 2 * (KL + 1) + KH + 1; r += T) {
     double v = 0.0;
     int slot;
     if (r < KL + 1) {
       int c = 0;
-#pragma unroll 16
-      for (int t = 0; t < T; ++t) c += bins.cnt[r * B::kRow + t];
+      for (int w = 0; w < kWaves; ++w) c += wcnt[w][r];
       v = (double)c;
       slot = S::kCount + r;
     } else if (r < 2 * (KL + 1)) {
       const int j = r - (KL + 1);
-#pragma unroll 16
-      for (int t = 0; t < T; ++t) v += bins.val[j * B::kRow + t];
+      for (int w = 0; w < kWaves; ++w) v += wval[w][j];
       slot = S::kDen + j;
     } else {
       const int j = r - 2 * (KL + 1);
-#pragma unroll 16
-      for (int t = 0; t < T; ++t) v += bins.val[(B::kNum0 + j) * B::kRow + t];
+      for (int w = 0; w < kWaves; ++w) v += wval[w][B::kNum0 + j];
       slot = S::kNum + j;
     }
     p.partials[(int64_t)slot * p.blocks + out] = v;
   }
+}
+
+// Inclusive prefix sums of tot[0 .. n) (n <= 64), lane k getting tot[0] +
+// ... + tot[k] summed in index order: the values go to lanes once, then
+// one running sum walks them (every lane computes the same sum from
+// readlanes) and lane k keeps its prefix.  No lane-dependent loop of LDS
+// reads.
+__device__ __forceinline__ double prefix_in_order(const double* tot, int n) {
+  const int lane = threadIdx.x & 63;
+  const double v = lane < n ? tot[lane] : 0.0;
+  double run = 0.0, mine = 0.0;
+  for (int j = 0; j < n; ++j) {
+    run += readlane_f64(v, j);
+    mine = lane == j ? run : mine;
+  }
+  return mine;
 }
 
 __device__ __forceinline__ double smooth_update(double b, double b_star, double delta) {
@@ -340,9 +393,9 @@ __global__ __launch_bounds__(1024) void clip_search_kernel(ClipArgs p) {
     // #(r_FP8 <= L_k) = the negative tokens in bins 0 .. k; the first k
     // with the least distance wins (key: distance, then k)
     uint64_t key = ~0ull;
+    // (the counts are exact in float64, so their prefix sums are too)
+    const int64_t below = (int64_t)prefix_in_order(tot + S::kCount, p.nl);
     if (lane < p.nl) {
-      int64_t below = 0;
-      for (int j = 0; j <= lane; ++j) below += (int64_t)tot[S::kCount + j];
       const int64_t d = below > cnt_ref ? below - cnt_ref : cnt_ref - below;
       key = ((uint64_t)d << 8) | (uint64_t)lane;
     }
@@ -354,7 +407,10 @@ __global__ __launch_bounds__(1024) void clip_search_kernel(ClipArgs p) {
     // Eq. 5 denominator at L*: the negative tokens with r_FP8 > L*, bins
     // kl + 1 .. nl, in bin order
     double den = 0.0;
-    for (int j = kl + 1; j <= p.nl; ++j) den += tot[S::kDen + j];
+    {
+      const double v = lane <= p.nl ? tot[S::kDen + lane] : 0.0;
+      for (int j = kl + 1; j <= p.nl; ++j) den += readlane_f64(v, j);
+    }
     den = fabs(den);
     const double den_ref = fabs(tot[4]);
     if (den_ref > 0.0 && den > 0.0) {
@@ -365,9 +421,8 @@ __global__ __launch_bounds__(1024) void clip_search_kernel(ClipArgs p) {
       // like its value
       double rho = 0.0;
       uint64_t dbits = ~0ull;
+      const double num = prefix_in_order(tot + S::kNum, p.nh);
       if (lane < p.nh) {
-        double num = 0.0;
-        for (int j = 0; j <= lane; ++j) num += tot[S::kNum + j];
         rho = fabs(num) / den;
         dbits = __double_as_longlong(fabs(rho - rho_ref));
       }
@@ -403,11 +458,11 @@ int clip_slots(int nl, int nh) {
 }
 
 hipError_t launch_calibrate_clip(const ClipArgs& p, hipStream_t s) {
-  // the paper's grids (21 and 41 points) get their own instantiation, 256
-  // threads a block; any grid up to kClipMaxL / kClipMaxH points takes the
-  // general one, 128 threads a block (its bins fill more LDS per thread)
-  if (p.nl <= 21 && p.nh <= 41) return clip_detail::launch<21, 41, 256>(p, s);
-  return clip_detail::launch<kClipMaxL, kClipMaxH, 128>(p, s);
+  // the paper's grids (21 and 41 points) get their own instantiation; any
+  // grid up to kClipMaxL / kClipMaxH points takes the general one; 768
+  // threads a block (three waves per SIMD)
+  if (p.nl <= 21 && p.nh <= 41) return clip_detail::launch<21, 41, 768>(p, s);
+  return clip_detail::launch<kClipMaxL, kClipMaxH, 768>(p, s);
 }
 
 }  // namespace fp8q
