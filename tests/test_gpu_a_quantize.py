@@ -100,6 +100,28 @@ def test_padded_codes_multi_tile(g, transposed):
     assert torch.all(buf[:, length:] == 0x5A)
 
 
+@pytest.mark.parametrize("g", [fp8q.BLOCK_128x1, fp8q.BLOCK_128x128, fp8q.BLOCK_1x128, fp8q.COL])
+def test_transposed_odd_tile_rows(g):
+    """Transposed output over an odd number of 128-row tiles (384 rows),
+    into a code array and a scale array with guard bands on both sides:
+    nothing outside them is written."""
+    rows, cols = 384, 256
+    x = synth.activations(rows, cols, seed=51 + g, outlier_seed=52 + g)
+    n = rows * cols
+    buf = torch.full((n + 8192,), 0xA5, dtype=torch.uint8, device=DEV)
+    codes = buf[4096:4096 + n].view(cols, rows)
+    ns = fp8q.scales_count(rows, cols, g, True)
+    sbuf = torch.full((ns + 256,), -7.0, dtype=torch.float32, device=DEV)
+    scales = sbuf[128:128 + ns]
+    fp8q.quantize(x.to(DEV), g, True, codes=codes, scales=scales)
+    torch.cuda.synchronize()
+    oc, os_ = _par.quantize(synth.bf16_bits(x), g, True)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint32), os_.view(np.uint32))
+    assert np.array_equal(codes.cpu().numpy(), oc)
+    assert torch.all(buf[:4096] == 0xA5) and torch.all(buf[4096 + n:] == 0xA5)
+    assert torch.all(sbuf[:128] == -7.0) and torch.all(sbuf[128 + ns:] == -7.0)
+
+
 def test_special_blocks():
     """All-zero, signed-zero, single-nonzero, constant-magnitude and
     subnormal-amax blocks, each a 1x128 block of one row."""
