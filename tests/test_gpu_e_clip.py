@@ -105,3 +105,63 @@ def test_deterministic():
         fp8q.calibrate_clip(*(b[k] for k in KEYS), 0.6, 1.8, result=r)
     torch.cuda.synchronize()
     assert torch.equal(res[0], res[1])
+
+
+def _result_dict(buf):
+    """The fp8q_clip_result fields of an 80-byte device buffer."""
+    raw = buf.cpu().numpy().tobytes()
+    f = np.frombuffer(raw[:56], dtype=np.float64)
+    i = np.frombuffer(raw[56:72], dtype=np.int64)
+    u = np.frombuffer(raw[72:80], dtype=np.int32)
+    return dict(zip(("l_new", "h_new", "l_star", "h_star", "alpha_low", "rho_bf16", "rho_fp8"), f.tolist()),
+                n_neg=int(i[0]), n_pos=int(i[1]), l_updated=int(u[0]), h_updated=int(u[1]))
+
+
+def test_stale_and_reused_workspace():
+    """A workspace full of stale bytes, then reused for a batch of another
+    size (another block count) and again: the oracle's answer each time."""
+    big = synth.rl_batch(64, 8, seed=71, fp8_sigma=0.1)
+    small = synth.rl_batch(8, 8, seed=72, fp8_sigma=0.1)
+    need = fp8q.lib().fp8q_calibrate_clip_workspace(big["adv"].numel())
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device=DEV)
+    for b, label in ((big, "stale workspace"), (small, "reused workspace"), (big, "reused again")):
+        print("calibrated clipping", label, b["adv"].numel(), "tokens", flush=True)
+        res = torch.empty(80, dtype=torch.uint8, device=DEV)
+        fp8q.calibrate_clip(*(b[k].to(DEV) for k in KEYS), 0.6, 1.8, workspace=ws, result=res, read=False)
+        torch.cuda.synchronize()
+        got = _result_dict(res)
+        want = clip.calibrate(*(b[k].numpy() for k in KEYS), 0.6, 1.8, clip.PAPER_CONFIG)
+        assert got["n_neg"] == want["n_neg"] and got["n_pos"] == want["n_pos"]
+        assert got["l_new"] == want["l_new"] and got["h_new"] == want["h_new"]
+        assert got["l_star"] == want["l_star"] and got["h_star"] == want["h_star"]
+
+
+def test_graph_replays():
+    """Captured in a HIP graph and replayed three times, with eager calls on
+    other data through the same workspace in between: every replay gives
+    the eager result."""
+    b = {k: v.to(DEV) for k, v in synth.rl_batch(32, 8, seed=81, fp8_sigma=0.1).items()}
+    other = {k: v.to(DEV) for k, v in synth.rl_batch(16, 8, seed=82).items()}
+    need = fp8q.lib().fp8q_calibrate_clip_workspace(b["adv"].numel())
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    eager = torch.empty(80, dtype=torch.uint8, device=DEV)
+    fp8q.calibrate_clip(*(b[k] for k in KEYS), 0.6, 1.8, workspace=ws, result=eager, read=False)
+    torch.cuda.synchronize()
+    res = torch.full((80,), 0x5A, dtype=torch.uint8, device=DEV)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            fp8q.calibrate_clip(*(b[k] for k in KEYS), 0.6, 1.8, workspace=ws, result=res, read=False)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    scratch = torch.empty(80, dtype=torch.uint8, device=DEV)
+    for rep in range(3):
+        print("graph replay", rep, flush=True)
+        res.fill_(0x5A)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(res, eager), rep
+        fp8q.calibrate_clip(*(other[k] for k in KEYS), 0.6, 1.8, workspace=ws, result=scratch, read=False)
+        torch.cuda.synchronize()
