@@ -380,8 +380,6 @@ __global__ __launch_bounds__(kThreads) void quant_dual_kernel(DualArgs d) {
   if (rg < 8 && cj < a.cols) d.scales_t[tr * a.cols + cj] = mine.s;
 }
 
-// Amax pass of the two-pass granularities: atomic max of |x| into `scales`
-// (zeroed beforehand) per tensor, row or column.
 // Partial maxima of the multi-tile granularities: float i sits at float
 // i % per of line i / per, lines being `ld` bytes apart.  In the code array
 // a line is one of its rows (columns when transposed) and holds per = its
