@@ -39,6 +39,9 @@ def parse():
                    help="skip the timings of the kernels outside the step (backward-pass quantizer)")
     p.add_argument("--cpu-rows", type=int, default=4096,
                    help="rows of X the oracle processes for the CPU baseline")
+    p.add_argument("--sweep", action="store_true",
+                   help="instead of the step's line: one JSON line per FFN up-projection shape of "
+                        "the 8B, 14B and 32B models at 4096, 8192 and 16384 tokens")
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
                    help="after timing, run one plain device-to-device copy of this many "
                         "MiB: a kernel of known traffic to scale HBM byte counters by")
@@ -347,6 +350,62 @@ def clock_under_load(torch, f, seconds=1.0):
             pass
 
 
+# FFN up-projection (hidden K -> intermediate N) of the model sizes the
+# paper's throughput comparison covers (Sec. 5.3): Qwen3-8B, Qwen3-14B, and
+# the 32B width used throughout (25600); token counts of 4K, 8K and 16K.
+SWEEP_MODELS = (("8b", 4096, 12288), ("14b", 5120, 17408), ("32b", 5120, 25600))
+SWEEP_TOKENS = (4096, 8192, 16384)
+
+
+def run_sweep(torch, fp8q, synth, dev, warmup=10, reps=30):
+    """The step (quantize X per 1x128, quantize W per 128x128, blockwise
+    GEMM) at each sweep shape, every kernel bracketed by HIP events as in
+    the main timing; one JSON line per shape."""
+    stream = torch.cuda.current_stream(dev)
+    for mi, (name, K, N) in enumerate(SWEEP_MODELS):
+        w = synth.weights(N, K, seed=synth.seed_for(10 + mi, 1), device=dev)
+        wq = torch.empty((N, K), dtype=torch.uint8, device=dev)
+        sw = torch.empty(fp8q.scales_count(N, K, fp8q.BLOCK_128x128), dtype=torch.float32, device=dev)
+        for M in SWEEP_TOKENS:
+            x = synth.activations(M, K, seed=synth.seed_for(10 + mi, 0), outlier_seed=synth.seed_for(10 + mi, 3),
+                                  device=dev)
+            xq = torch.empty((M, K), dtype=torch.uint8, device=dev)
+            sx = torch.empty(fp8q.scales_count(M, K, fp8q.BLOCK_1x128), dtype=torch.float32, device=dev)
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+
+            def step(ev=None):
+                if ev is not None:
+                    ev[0].record(stream)
+                fp8q.quantize(x, fp8q.BLOCK_1x128, codes=xq, scales=sx)
+                if ev is not None:
+                    ev[1].record(stream)
+                fp8q.quantize(w, fp8q.BLOCK_128x128, codes=wq, scales=sw)
+                if ev is not None:
+                    ev[2].record(stream)
+                fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y)
+                if ev is not None:
+                    ev[3].record(stream)
+
+            for _ in range(warmup):
+                step()
+            events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+            for ev in events:
+                step(ev)
+            torch.cuda.synchronize()
+            avg = lambda a, b: sum(e[a].elapsed_time(e[b]) for e in events) / reps * 1000.0
+            t_qx, t_qw, t_g = avg(0, 1), avg(1, 2), avg(2, 3)
+            flops = 2.0 * M * N * K
+            print(json.dumps({
+                "sweep": "%s_ffn_up_fwd_blockwise" % name, "M": M, "K": K, "N": N,
+                "gemm_us": round(t_g, 1), "gemm_tflops": round(flops / t_g * 1e-6, 1),
+                "gemm_frac_fp8_peak": round(flops / t_g * 1e-6 / PEAK_FP8_TFLOPS, 4),
+                "quantize_x_us": round(t_qx, 1), "quantize_w_us": round(t_qw, 1),
+                "step_us": round(t_qx + t_qw + t_g, 1),
+                "step_tflops": round(flops / (t_qx + t_qw + t_g) * 1e-6, 1)}), flush=True)
+            del x, xq, sx, y
+        del w, wq, sw
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -361,6 +420,9 @@ def main():
 
     M, K, N = WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
+    if args.sweep:
+        run_sweep(torch, fp8q, synth, dev)
+        return
     x = synth.activations(M, K, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=dev)
     w = synth.weights(N, K, seed=synth.seed_for(2, 1), device=dev)
     xq = torch.empty((M, K), dtype=torch.uint8, device=dev)
