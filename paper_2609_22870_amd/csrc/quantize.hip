@@ -423,21 +423,36 @@ __global__ __launch_bounds__(kThreads) void amax_tile_kernel(QuantArgs a, Partia
 }
 
 // S of each unit from its partials (those of unit u at u, u + units, ...):
-// a workgroup takes 64 units, its four waves split the partials, and LDS
-// joins the waves.
+// a workgroup takes 64 units and its sixteen waves split the partials,
+// eight loads in flight per lane at a time (a column's 128 partials of a
+// 16384-row input are then one round of loads, not a chain of 32), and LDS
+// joins the waves.  A max is exact in any order.
+constexpr int kReduceWaves = 16, kReduceDepth = 8;
+
 template <bool E5>
-__global__ __launch_bounds__(256) void reduce_units_kernel(Partials part, int64_t units, int64_t nparts,
-                                                          float* scales, int pow2) {
-  __shared__ float lds[4][64];
+__global__ __launch_bounds__(kReduceWaves * 64) void reduce_units_kernel(Partials part, int64_t units,
+                                                                        int64_t nparts, float* scales, int pow2) {
+  __shared__ float lds[kReduceWaves][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t u = (int64_t)blockIdx.x * 64 + lane;
   float m = 0.0f;
-  if (u < units)
-    for (int64_t p = wave; p < nparts; p += 4) m = fmaxf(m, *part.at(p * units + u));
+  if (u < units) {
+    for (int64_t p0 = wave; p0 < nparts; p0 += kReduceWaves * kReduceDepth) {
+      float v[kReduceDepth];
+#pragma unroll
+      for (int j = 0; j < kReduceDepth; ++j) {
+        const int64_t pj = p0 + (int64_t)kReduceWaves * j;
+        v[j] = pj < nparts ? *part.at(pj * units + u) : 0.0f;
+      }
+#pragma unroll
+      for (int j = 0; j < kReduceDepth; ++j) m = fmaxf(m, v[j]);
+    }
+  }
   lds[wave][lane] = m;
   __syncthreads();
   if (wave == 0 && u < units) {
-    m = fmaxf(fmaxf(lds[0][lane], lds[1][lane]), fmaxf(lds[2][lane], lds[3][lane]));
+#pragma unroll
+    for (int w = 1; w < kReduceWaves; ++w) m = fmaxf(m, lds[w][lane]);
     scales[u] = unit_scale_fmt<E5>(m, pow2 != 0).s;
   }
 }
@@ -587,7 +602,8 @@ hipError_t launch_two_pass(const QuantArgs& a, bool trans, hipStream_t s) {
     const dim3 grid((unsigned)tiles_c, (unsigned)tiles_r);
     amax_tile_kernel<K><<<grid, kThreads, 0, s>>>(a, part);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    reduce_units_kernel<E5><<<(unsigned)((units + 63) / 64), 256, 0, s>>>(part, units, nparts, a.scales, a.pow2);
+    reduce_units_kernel<E5><<<(unsigned)((units + 63) / 64), kReduceWaves * 64, 0, s>>>(part, units, nparts, a.scales,
+                                                                                       a.pow2);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   return trans ? launch_tile<K, true, E5>(a, s) : launch_tile<K, false, E5>(a, s);
