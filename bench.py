@@ -248,12 +248,12 @@ def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
             probs.append((xq, sx, wq_i, sw_i))
         outs = fp8q.gemm_grouped(probs, fp8q.BLOCK_1x128, fp8q.BLOCK_128x128)
         t_grp = timed(lambda: fp8q.gemm_grouped(probs, fp8q.BLOCK_1x128, fp8q.BLOCK_128x128, outs=outs))
-        t_sep = timed(lambda: [fp8q.gemm(a, sa, fp8q.BLOCK_1x128, b, sb, fp8q.BLOCK_128x128, out=c)
-                               for (a, sa, b, sb), c in zip(probs, outs)])
+        t_calls = timed(lambda: [fp8q.gemm(a, sa, fp8q.BLOCK_1x128, b, sb, fp8q.BLOCK_128x128, out=c)
+                                 for (a, sa, b, sb), c in zip(probs, outs)])
         flops = 2.0 * M * K * sum(widths)
         grouped[kind] = {"widths": list(widths), "us": round(t_grp, 1),
                          "tflops": round(flops / (t_grp * 1e-6) / 1e12, 1),
-                         "separate_calls_us": round(t_sep, 1)}
+                         "separate_calls_us": round(t_calls, 1)}
         del probs, outs
 
     rl = {k: v.to(dev) for k, v in synth.rl_batch(**synth.RL_BATCH, seed=5001).items()}
