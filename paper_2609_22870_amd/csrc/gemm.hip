@@ -380,7 +380,14 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   const int wave = KS > 1 ? uniform(wave_all % kWaves) : wave_all;  // within the group
   const int wm = (wave / kWavesN) * WM, wn = (wave % kWavesN) * WN;
   const int KT = (int)(g.K / kBK) / KS;  // steps of this group (KS divides K / 128)
-  auto kb = [&](int st) { return st * KS + kg; };  // K block of the group's step st
+  // K block of the group's step st.  Tiles whose first column lies in an
+  // odd 1024-column band walk K backwards: the 256 x 256 raster runs 8 tile
+  // rows x 4 tile columns (one band) on an XCD at a time and then the next
+  // band of the same rows, which so starts on the K blocks of A the last one
+  // ended with, still in L2.  Every tile shape takes the same direction for
+  // an output element, so a grouped launch sums as a single call would.
+  const bool rev = ((n0 >> 10) & 1) != 0;
+  auto kb = [&](int st) { return (rev ? KT - 1 - st : st) * KS + kg; };
   const int mw = (int)m0 + wm, nw = (int)n0 + wn;  // wave's first row / column
 
   v4f acc[TI][TJ];
