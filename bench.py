@@ -37,11 +37,21 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-extras", action="store_true",
                    help="skip the timings of the kernels outside the step (backward-pass quantizer)")
-    p.add_argument("--cpu-rows", type=int, default=4096,
-                   help="rows of X the oracle processes for the CPU baseline")
+    p.add_argument("--cpu-rows", type=int, default=2048,
+                   help="rows of Y the oracle's exact GEMM computes for the CPU baseline")
     p.add_argument("--sweep", action="store_true",
                    help="instead of the step's line: one JSON line per FFN up-projection shape of "
                         "the 8B, 14B and 32B models at 4096, 8192 and 16384 tokens")
+    p.add_argument("--config", type=int, choices=(1, 2, 3, 4, 5), default=None,
+                   help="instead of the step's line: one JSON line per quantizer and GEMM of one "
+                        "of the five workloads (1 tiny per-tensor, 2 8B blockwise forward, 3 8B "
+                        "rowwise, 4 decode, 5 32B training layers), each its median over timed "
+                        "repetitions, with the last-level cache flushed before each repetition of "
+                        "the HBM-bound kernels")
+    p.add_argument("--reps", type=int, default=50, help="timed repetitions per kernel with --config")
+    p.add_argument("--settle-s", type=float, default=1.0,
+                   help="seconds of untimed steps before the warmup steps, so that the timed "
+                        "steps run at the clock the GPU holds under this load")
     p.add_argument("--calibrate-copy-mib", type=int, default=0,
                    help="after timing, run one plain device-to-device copy of this many "
                         "MiB: a kernel of known traffic to scale HBM byte counters by")
@@ -85,11 +95,30 @@ def recorded_traffic(workload):
         return None
 
 
+def host_cpu():
+    """nproc, the cores this process may use and the CPU model name."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity_cores": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
 def cpu_baseline(x, w, M, K, N, rows):
-    """The oracle (untuned) on a sample of the same step: `rows` rows of X
-    quantized 1x128, the matching share of W's rows (rounded up to whole
-    128-row blocks) quantized 128x128, and those rows of Y computed exactly.
-    Runs on all host cores, one oracle call per thread."""
+    """The oracle (untuned) on the host cores:
+    * quantizers on the full tensors of the step: X [M, K] per 1x128 block
+      and W [N, K] per 128x128 block, on one thread and on all cores (the
+      rows split into contiguous chunks of whole units, one oracle call per
+      chunk; the oracle's ctypes calls release the GIL);
+    * the exact GEMM on `rows` rows of Y spread over all of M, on all cores,
+      and its time for all M rows extrapolated from them (labelled so).
+    value: the step's flops over the all-core step time (both quantizers on
+    the full tensors plus the extrapolated GEMM)."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -98,45 +127,58 @@ def cpu_baseline(x, w, M, K, N, rows):
     from paper_2609_22870_amd import synth
 
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
-    xs = synth.bf16_bits(x[:rows])
-    wrows = max(128, ((N * rows // M + 127) // 128) * 128)
+    xs = synth.bf16_bits(x)
     wb = synth.bf16_bits(w)
+    qbytes = lambda r, c, n_scales: 3.0 * r * c + 4.0 * n_scales
+
     t0 = time.perf_counter()
+    ox, osx = oracle.quantize(xs, oracle.BLOCK_1x128)
+    tx1 = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    ow, osw = oracle.quantize(wb, oracle.BLOCK_128x128)
+    tw1 = time.perf_counter() - t0
+
+    def chunks(n_rows, unit):
+        b = np.linspace(0, n_rows // unit, 4 * cores + 1).astype(np.int64) * unit
+        return [(int(a), int(c)) for a, c in zip(b[:-1], b[1:]) if c > a]
+
     with ThreadPoolExecutor(cores) as ex:
-        xparts = np.array_split(np.arange(rows), cores)
-        xres = list(ex.map(lambda r: oracle.quantize(xs[r[0]:r[-1] + 1], oracle.BLOCK_1x128), xparts))
-        wblocks = [(i, min(wrows, i + 128)) for i in range(0, wrows, 128)]
-        list(ex.map(lambda ab: oracle.quantize(wb[ab[0]:ab[1]], oracle.BLOCK_128x128), wblocks))
-    t_quant = time.perf_counter() - t0
-    # the GEMM rows need W quantized whole; that is not timed again (the W
-    # share above already stands for it at the sampled rate)
-    with ThreadPoolExecutor(cores) as ex:
-        wparts = list(ex.map(lambda i: oracle.quantize(wb[i:i + 128], oracle.BLOCK_128x128),
-                             range(0, N, 128)))
-    ow = np.concatenate([c for c, _ in wparts])
-    osw = np.concatenate([s for _, s in wparts])
-    t1 = time.perf_counter()
-    with ThreadPoolExecutor(cores) as ex:
-        def rows_of(i):
-            codes, scales = xres[i]
-            n = codes.shape[0]
-            return oracle.gemm_rows(codes, scales, oracle.BLOCK_1x128, ow, osw,
-                                    oracle.BLOCK_128x128, np.arange(n))
-        list(ex.map(rows_of, range(len(xres))))
-    t_gemm = time.perf_counter() - t1
-    # the sampled share of one step: rows/M of the GEMM and of X, wrows/N of W
-    t_step = t_gemm + t_quant
-    flops = 2.0 * rows * N * K
-    return {
-        "value": flops / t_step / 1e12,
+        t0 = time.perf_counter()
+        list(ex.map(lambda ab: oracle.quantize(xs[ab[0]:ab[1]], oracle.BLOCK_1x128), chunks(M, 1)))
+        txn = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        list(ex.map(lambda ab: oracle.quantize(wb[ab[0]:ab[1]], oracle.BLOCK_128x128), chunks(N, 128)))
+        twn = time.perf_counter() - t0
+        sample = np.linspace(0, M - 1, rows).astype(np.int64)
+        t0 = time.perf_counter()
+        list(ex.map(lambda r: oracle.gemm_rows(ox, osx, oracle.BLOCK_1x128, ow, osw, oracle.BLOCK_128x128, r),
+                    np.array_split(sample, 4 * cores)))
+        tg = time.perf_counter() - t0
+    tg_full = tg * M / rows
+    flops = 2.0 * M * N * K
+    xb, wbytes = qbytes(M, K, osx.size), qbytes(N, K, osw.size)
+    out = {
+        "value": flops / (txn + twn + tg_full) / 1e12,
         "unit": "TFLOP/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": "%d of %d rows of Y = X W^T (exact int64/binary128 oracle GEMM), "
-                  "those rows of X quantized 1x128 and %d of %d rows of W quantized "
-                  "128x128; %.1f s wall (%.1f s quantize, %.1f s GEMM)"
-                  % (rows, M, wrows, N, t_step, t_quant, t_gemm),
+        "sample": "quantizers on the full X [%d, %d] (1x128) and W [%d, %d] (128x128); exact "
+                  "int64/binary128 GEMM on %d of %d rows of Y = X W^T spread over M, its full "
+                  "time extrapolated; value = 2MNK over the all-core quantizers plus the "
+                  "extrapolated GEMM" % (M, K, N, K, rows, M),
+        "quantize_x_1x128": {"one_thread_s": round(tx1, 3), "one_thread_gbs": round(xb / tx1 / 1e9, 3),
+                             "all_cores_s": round(txn, 3), "all_cores_gbs": round(xb / txn / 1e9, 3),
+                             "elements_per_s_all_cores": round(M * K / txn)},
+        "quantize_w_128x128": {"one_thread_s": round(tw1, 3), "one_thread_gbs": round(wbytes / tw1 / 1e9, 3),
+                               "all_cores_s": round(twn, 3), "all_cores_gbs": round(wbytes / twn / 1e9, 3),
+                               "elements_per_s_all_cores": round(N * K / twn)},
+        "gemm_sample_rows": rows,
+        "gemm_sample_s": round(tg, 3),
+        "gemm_mac_per_s": round(rows * N * K / tg),
+        "gemm_full_extrapolated_s": round(tg_full, 1),
     }
+    out.update(host_cpu())
+    return out
 
 
 def time_extras(torch, fp8q, synth, dev, x, w, xq, sx, wq, sw, reps=20):
@@ -406,6 +448,161 @@ def run_sweep(torch, fp8q, synth, dev, warmup=10, reps=30):
         del w, wq, sw
 
 
+class Flush:
+    """A 512 MiB device copy (1 GiB of HBM traffic, four times the 256 MB
+    last-level cache) run before a repetition, outside its events, so that
+    the kernel timed next reads its operands from HBM."""
+
+    def __init__(self, torch, dev):
+        self.src = torch.zeros(512 << 20, dtype=torch.uint8, device=dev)
+        self.dst = torch.empty_like(self.src)
+
+    def __call__(self):
+        self.dst.copy_(self.src)
+
+
+def time_op(torch, stream, f, reps, warmup=10, flush=None):
+    """Sorted durations in us of `reps` calls of f, each bracketed by HIP
+    events on the launch stream, after `warmup` untimed calls; with flush,
+    flush() runs before every call, outside the events."""
+    for _ in range(warmup):
+        if flush is not None:
+            flush()
+        f()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for s, e in evs:
+        if flush is not None:
+            flush()
+        s.record(stream)
+        f()
+        e.record(stream)
+    torch.cuda.synchronize()
+    return sorted(s.elapsed_time(e) * 1000.0 for s, e in evs)
+
+
+def percentiles(ts):
+    n = len(ts)
+    return ts[min(n - 1, int(0.1 * n))], ts[n // 2], ts[min(n - 1, int(0.9 * n))]
+
+
+GRAN_NAMES = {0: "tensor", 1: "row", 2: "col", 3: "1x128", 4: "128x1", 5: "128x128"}
+
+
+def run_config(torch, fp8q, synth, dev, cfg, reps):
+    """One JSON line per quantizer and GEMM of workload `cfg` (the five
+    workloads of the parity tests, at full size), each the median and
+    p10 / p90 over `reps` event-timed repetitions after 10 untimed ones.
+    Quantizers and the HBM-bound decode GEMMs run with the last-level cache
+    flushed before every repetition; the MFMA-bound GEMMs back to back.
+    Rates: quantizer bytes are 2 (bf16 read) + 1 per code written + 4 per
+    scale; GEMM bytes MK + NK + 2MN + 4 per scale; GEMM work 2MNK flops."""
+    stream = torch.cuda.current_stream(dev)
+    flush = Flush(torch, dev)
+    names = {1: "tiny_tensorwise", 2: "8b_ffn_up_fwd_blockwise", 3: "8b_rowwise", 4: "8b_decode_blockwise",
+             5: "32b_train_blockwise"}
+
+    def emit(op, ts, bound, work, unit_peak, extra):
+        p10, p50, p90 = percentiles(ts)
+        line = {"config": cfg, "workload": names[cfg], "op": op, "us_p50": round(p50, 2),
+                "us_p10": round(p10, 2), "us_p90": round(p90, 2), "reps": len(ts), "bound": bound}
+        if bound == "hbm":
+            rate = work / (p50 * 1e-6) / 1e9
+            line.update({"gbs": round(rate, 1), "frac_hbm": round(rate / PEAK_HBM_GBS, 4),
+                         "algorithmic_bytes": round(work)})
+        elif bound == "mfma":
+            rate = work / (p50 * 1e-6) / 1e12
+            line.update({"tflops": round(rate, 1), "frac_fp8_peak": round(rate / PEAK_FP8_TFLOPS, 4),
+                         "flops": round(work)})
+        else:
+            line.update({"flops": round(work)})
+        line.update(extra)
+        print(json.dumps(line), flush=True)
+
+    def quant(label, x, g, transposed=False, **kw):
+        codes, scales = fp8q.quantize(x, g, transposed, **kw)
+        ts = time_op(torch, stream, lambda: fp8q.quantize(x, g, transposed, codes=codes, scales=scales, **kw),
+                     reps, flush=flush)
+        rows, cols = x.shape
+        emit("quantize " + label, ts, "hbm", 3.0 * rows * cols + 4.0 * scales.numel(),
+             PEAK_HBM_GBS, {"shape": [rows, cols], "granularity": GRAN_NAMES[g], "transposed": transposed,
+                            "flushed": True})
+        return codes, scales
+
+    def dual(label, x):
+        outs = fp8q.quantize_dual(x)
+        ts = time_op(torch, stream, lambda: fp8q.quantize_dual(x, *outs), reps, flush=flush)
+        rows, cols = x.shape
+        emit("quantize_dual " + label, ts, "hbm", 4.0 * rows * cols + 4.0 * (outs[1].numel() + outs[3].numel()),
+             PEAK_HBM_GBS, {"shape": [rows, cols], "granularity": "1x128 + 128x1 transposed", "flushed": True})
+        return outs
+
+    def gemm(label, a, sa, ga, b, sb, gb, hbm=False):
+        M, K = a.shape
+        N = b.shape[0]
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        f = lambda: fp8q.gemm(a, sa, ga, b, sb, gb, out=out)
+        flops = 2.0 * M * N * K
+        nbytes = 1.0 * M * K + 1.0 * N * K + 2.0 * M * N + 4.0 * (sa.numel() + sb.numel())
+        extra = {"shape_mkn": [M, K, N], "scaling": "%s x %s" % (GRAN_NAMES[ga], GRAN_NAMES[gb]),
+                 "flushed": hbm}
+        if hbm:
+            ts = time_op(torch, stream, f, reps, flush=flush)
+            warm = percentiles(time_op(torch, stream, f, reps))[1]
+            extra["tflops_at_p50"] = round(flops / (percentiles(ts)[1] * 1e-6) / 1e12, 1)
+            extra["us_p50_back_to_back"] = round(warm, 2)
+            emit("gemm " + label, ts, "hbm", nbytes, PEAK_HBM_GBS, extra)
+        elif cfg == 1:
+            emit("gemm " + label, time_op(torch, stream, f, reps), "launch", flops, None, extra)
+        else:
+            extra["algorithmic_bytes"] = round(nbytes)
+            emit("gemm " + label, time_op(torch, stream, f, reps), "mfma", flops, PEAK_FP8_TFLOPS, extra)
+        del out
+
+    if cfg == 1:
+        a = synth.normal_bf16((128, 256), 1.0, synth.seed_for(1, 0), dev)
+        b = synth.normal_bf16((256, 256), 0.02, synth.seed_for(1, 1), dev)
+        A, sA = quant("A", a, fp8q.TENSOR)
+        B, sB = quant("B", b, fp8q.TENSOR)
+        gemm("tiny", A, sA, fp8q.TENSOR, B, sB, fp8q.TENSOR)
+    elif cfg == 2:
+        M, K, N = synth.WORKLOADS["8b_ffn_up_fwd_blockwise"]["shapes"][0]
+        x = synth.activations(M, K, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=dev)
+        w = synth.weights(N, K, seed=synth.seed_for(2, 1), device=dev)
+        X, sX = quant("X", x, fp8q.BLOCK_1x128)
+        W, sW = quant("W", w, fp8q.BLOCK_128x128)
+        gemm("fwd", X, sX, fp8q.BLOCK_1x128, W, sW, fp8q.BLOCK_128x128)
+    elif cfg in (3, 4):
+        key = "8b_rowwise" if cfg == 3 else "8b_decode_blockwise"
+        gx, gw = (fp8q.ROW, fp8q.ROW) if cfg == 3 else (fp8q.BLOCK_1x128, fp8q.BLOCK_128x128)
+        for i, (M, K, N) in enumerate(synth.WORKLOADS[key]["shapes"]):
+            x = synth.activations(M, K, seed=synth.seed_for(cfg, 0, i), outlier_seed=synth.seed_for(cfg, 3, i),
+                                  device=dev)
+            w = synth.weights(N, K, seed=synth.seed_for(cfg, 1, i), device=dev)
+            tag = "%dx%dx%d" % (M, K, N)
+            X, sX = quant("X " + tag, x, gx)
+            W, sW = quant("W " + tag, w, gw)
+            gemm(tag, X, sX, gx, W, sW, gw, hbm=(cfg == 4))
+            del x, w, X, sX, W, sW
+    else:
+        T = 16384
+        for si, proj, k_in, n_out in ((0, "up", 5120, 25600), (3, "down", 25600, 5120)):
+            x = synth.activations(T, k_in, seed=synth.seed_for(5, 0, si), outlier_seed=synth.seed_for(5, 3, si),
+                                  device=dev)
+            w = synth.weights(n_out, k_in, seed=synth.seed_for(5, 1, si), device=dev)
+            dy = synth.grads(T, n_out, seed=synth.seed_for(5, 2, si), device=dev)
+            X, sX = quant(proj + " X (fwd)", x, fp8q.BLOCK_1x128)
+            W, sW = quant(proj + " W (fwd)", w, fp8q.BLOCK_128x128)
+            Wt, sWt = quant(proj + " W^T (dgrad)", w, fp8q.BLOCK_128x128, transposed=True)
+            dY, sdY, dYt, sdYt = dual(proj + " dY (dgrad, wgrad)", dy)
+            Xt, sXt = quant(proj + " X^T (wgrad)", x, fp8q.BLOCK_128x1, transposed=True)
+            gemm(proj + " fwd", X, sX, fp8q.BLOCK_1x128, W, sW, fp8q.BLOCK_128x128)
+            del X, sX, W, sW
+            gemm(proj + " dgrad", dY, sdY, fp8q.BLOCK_1x128, Wt, sWt, fp8q.BLOCK_128x128)
+            del dY, sdY, Wt, sWt
+            gemm(proj + " wgrad", Xt, sXt, fp8q.BLOCK_1x128, dYt, sdYt, fp8q.BLOCK_1x128)
+            del x, w, dy, Xt, sXt, dYt, sdYt
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -422,6 +619,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.sweep:
         run_sweep(torch, fp8q, synth, dev)
+        return
+    if args.config is not None:
+        run_config(torch, fp8q, synth, dev, args.config, args.reps)
         return
     x = synth.activations(M, K, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=dev)
     w = synth.weights(N, K, seed=synth.seed_for(2, 1), device=dev)
@@ -445,6 +645,16 @@ def main():
         if ev is not None:
             ev[3].record(stream)
 
+    # untimed steps for --settle-s seconds first: the shader clock ramps and
+    # then settles under the power limit over the first tens of milliseconds
+    # of load, so the timed steps run at the clock this load holds
+    settle_steps = 0
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < args.settle_s:
+        for _ in range(10):
+            step()
+        settle_steps += 10
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -504,7 +714,22 @@ def main():
                          "hbm_peak": PEAK_HBM_GBS},
         "gemm_us_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
         "timed_wall_s": round(wall, 3),
+        "settle": {"seconds": args.settle_s, "untimed_steps": settle_steps},
     }
+    # the quantizers alone with the last-level cache flushed before each
+    # repetition (their in-step figures above may find part of their input
+    # there): median over 50
+    flush = Flush(torch, dev)
+    tqx = percentiles(time_op(torch, stream, lambda: fp8q.quantize(x, fp8q.BLOCK_1x128, codes=xq, scales=sx),
+                              50, flush=flush))[1]
+    tqw = percentiles(time_op(torch, stream, lambda: fp8q.quantize(w, fp8q.BLOCK_128x128, codes=wq, scales=sw),
+                              50, flush=flush))[1]
+    del flush
+    out["quantize_flushed"] = {
+        "x_1x128_us": round(tqx, 2), "x_1x128_gbs": round(qx_bytes / (tqx * 1e-6) / 1e9, 1),
+        "x_1x128_frac_hbm": round(qx_bytes / (tqx * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+        "w_128x128_us": round(tqw, 2), "w_128x128_gbs": round(qw_bytes / (tqw * 1e-6) / 1e9, 1),
+        "w_128x128_frac_hbm": round(qw_bytes / (tqw * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     # the shader clock the GEMM runs at: its peak at that clock is the
     # dense FP8 rate scaled by clock / 2400 MHz
     clk = clock_under_load(torch, lambda: fp8q.gemm(xq, sx, fp8q.BLOCK_1x128, wq, sw, fp8q.BLOCK_128x128, out=y))

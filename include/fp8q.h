@@ -24,7 +24,9 @@
  * never allocates, frees or synchronizes; every call enqueues its kernels on
  * `stream` (a hipStream_t; NULL is the legacy default stream) and returns.
  * Arguments are validated on the host before anything is enqueued; a
- * rejected call enqueues nothing.  Faults inside kernels surface at the
+ * rejected call enqueues nothing.  Sizes and leading dimensions above
+ * 2^31 - 1 elements (Calibrated Clipping batches above 2^52 tokens, casts
+ * above 2^62 values) are FP8Q_ERR_UNSUPPORTED.  Faults inside kernels surface at the
  * caller's next synchronization.  The library holds no mutable global
  * state, so calls from several threads are safe; calls that write the same
  * buffers must be ordered by the caller.
@@ -77,7 +79,9 @@ enum { FP8Q_E5M2 = 4u };
 
 /*
  * Number of fp32 scales fp8q_quantize writes for an input of rows x cols
- * with granularity g and `flags`; -1 if the arguments are invalid.
+ * with granularity g and `flags` (the scaling units of Eq. 3 for the
+ * granularities of Sec. 2.2); -1 if the arguments are invalid or a size
+ * exceeds 2^31 - 1.
  *
  * Scale layouts, for the OUTPUT matrix o[orows][ocols] (x, or x^T when
  * transposed) and the granularity g_o it sees (g, or g with rows and
@@ -323,9 +327,15 @@ fp8q_status fp8q_calibrate_clip(const float *adv, const float *w_tis,
                                 struct ihipStream_t *stream);
 
 /*
- * Q_FP8(RN32(x[i] / scale)) for n fp32 values with one explicit scale: the
- * device rounding routine of fp8q_quantize exposed for exhaustive checks.
- * x and codes need no alignment beyond their element size; scale > 0.
+ * Q_FP8(RN32(x[i] / scale)) for n fp32 values with one explicit scale (Eq.
+ * 3's rounding and clamping with S given): the clamp and the hardware
+ * E4M3 conversion that fp8q_quantize ends with, exposed for exhaustive
+ * checks.  The quotient here is an IEEE division, correctly rounded; the
+ * quantizers form the same correctly rounded quotient from a reciprocal
+ * and two fused multiply-adds (checked against the division over every
+ * bf16 amax and x pair on the host, and through the 1x128 quantizer on the
+ * GPU).  x and codes need no alignment beyond their element size;
+ * scale > 0.
  */
 fp8q_status fp8q_cast_f32(const float *x, int64_t n, float scale,
                           uint8_t *codes, struct ihipStream_t *stream);

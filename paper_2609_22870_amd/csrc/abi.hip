@@ -12,6 +12,14 @@ bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p
 
 bool valid_granularity(int g) { return g >= FP8Q_TENSOR && g <= FP8Q_BLOCK_128x128; }
 
+// Largest size or leading dimension taken (else FP8Q_ERR_UNSUPPORTED): every
+// product of two of them, doubled, stays below 2^63, so the checks and the
+// launchers' offset arithmetic cannot overflow.
+constexpr int64_t kMaxDim = 0x7fffffff;
+bool dims_ok(int64_t a, int64_t b, int64_t c = 1, int64_t d = 1, int64_t e = 1) {
+  return a <= kMaxDim && b <= kMaxDim && c <= kMaxDim && d <= kMaxDim && e <= kMaxDim;
+}
+
 constexpr unsigned kQuantFlags = FP8Q_OUT_TRANSPOSED | FP8Q_POW2_SCALE | FP8Q_E5M2;
 
 int transposed_granularity(int g) {
@@ -37,6 +45,9 @@ int64_t count_for(int64_t rows, int64_t cols, int g) {
 }
 
 fp8q_status from_hip(hipError_t e) { return e == hipSuccess ? FP8Q_OK : FP8Q_ERR_HIP; }
+
+// Largest batch of Calibrated Clipping (tokens; else FP8Q_ERR_UNSUPPORTED).
+constexpr int64_t kMaxClipTokens = (int64_t)1 << 52;
 
 // Calibrated Clipping: one block per `chunk` consecutive tokens, at most
 // kClipMaxBlocks (one per CU), chunks a multiple of 1024 tokens (up to 256
@@ -67,6 +78,7 @@ fp8q_status gemm_args(const uint8_t* A, const float* sA, fp8q_granularity gA, in
   if (formats & ~(unsigned)(FP8Q_A_E5M2 | FP8Q_B_E5M2)) return FP8Q_ERR_INVAL;
   if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
   if (lda < K || ldb < K || ldc < N) return FP8Q_ERR_INVAL;
+  if (!dims_ok(M, N, lda, ldb, ldc)) return FP8Q_ERR_UNSUPPORTED;
   if (gA == FP8Q_TENSOR && gB == FP8Q_TENSOR)
     pair = fp8q::kPairTensor;
   else if (gA == FP8Q_ROW && gB == FP8Q_ROW)
@@ -121,7 +133,7 @@ fp8q_status gemm_checked(const uint8_t* A, const float* sA, fp8q_granularity gA,
 extern "C" {
 
 int64_t fp8q_scales_count(int64_t rows, int64_t cols, fp8q_granularity g, unsigned flags) {
-  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~kQuantFlags))
+  if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~kQuantFlags) || !dims_ok(rows, cols))
     return -1;
   const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
   const int64_t orows = t ? cols : rows, ocols = t ? rows : cols;
@@ -135,6 +147,7 @@ fp8q_status fp8q_quantize(const void* x, int64_t rows, int64_t cols, int64_t ldx
   if (rows <= 0 || cols <= 0 || !valid_granularity(g) || (flags & ~kQuantFlags)) return FP8Q_ERR_INVAL;
   const bool t = (flags & FP8Q_OUT_TRANSPOSED) != 0;
   if (ldx < cols || ldc < (t ? rows : cols)) return FP8Q_ERR_INVAL;
+  if (!dims_ok(rows, cols, ldx, ldc)) return FP8Q_ERR_UNSUPPORTED;
   const bool splits_cols = g == FP8Q_BLOCK_1x128 || g == FP8Q_BLOCK_128x128;
   const bool splits_rows = g == FP8Q_BLOCK_128x1 || g == FP8Q_BLOCK_128x128;
   if (cols % 16 || (t && rows % 16)) return FP8Q_ERR_UNSUPPORTED;
@@ -162,6 +175,7 @@ fp8q_status fp8q_quantize_dual(const void* x, int64_t rows, int64_t cols, int64_
   if (!x || !codes_r || !scales_r || !codes_t || !scales_t) return FP8Q_ERR_INVAL;
   if (flags & ~(unsigned)(FP8Q_POW2_SCALE | FP8Q_E5M2)) return FP8Q_ERR_INVAL;
   if (rows <= 0 || cols <= 0 || ldx < cols || ldc_r < cols || ldc_t < rows) return FP8Q_ERR_INVAL;
+  if (!dims_ok(rows, cols, ldx, ldc_r, ldc_t)) return FP8Q_ERR_UNSUPPORTED;
   if (rows % 128 || cols % 128) return FP8Q_ERR_UNSUPPORTED;
   if (rows > (int64_t)65535 * 128) return FP8Q_ERR_UNSUPPORTED;  // grid.y limit
   if (!aligned(x, 16) || !aligned(codes_r, 16) || !aligned(codes_t, 16) || !aligned(scales_r, 4) ||
@@ -222,6 +236,7 @@ fp8q_status fp8q_gemm_pow2(const uint8_t* A, const float* sA, fp8q_granularity g
   if (!A || !sA || !B || !sB || !C) return FP8Q_ERR_INVAL;
   if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
   if (lda < K || ldb < K || ldc < N) return FP8Q_ERR_INVAL;
+  if (!dims_ok(M, N, lda, ldb, ldc)) return FP8Q_ERR_UNSUPPORTED;
   if (gA != FP8Q_BLOCK_1x128 || gB != FP8Q_BLOCK_128x128) return FP8Q_ERR_UNSUPPORTED;
   if (K % 128 || N % 128) return FP8Q_ERR_UNSUPPORTED;
   if (((M + 127) / 128) * (N / 128) > 0x7fffffff) return FP8Q_ERR_UNSUPPORTED;
@@ -259,6 +274,7 @@ fp8q_status fp8q_gemm_quantized(const uint8_t* A, const float* sA, fp8q_granular
   if (!A || !sA || !B || !sB || !codes || !scales) return FP8Q_ERR_INVAL;
   if (M <= 0 || N <= 0 || K <= 0 || !valid_granularity(gA) || !valid_granularity(gB)) return FP8Q_ERR_INVAL;
   if (lda < K || ldb < K || ldq < N) return FP8Q_ERR_INVAL;
+  if (!dims_ok(M, N, lda, ldb, ldq)) return FP8Q_ERR_UNSUPPORTED;
   if (gA != FP8Q_BLOCK_1x128 || gB != FP8Q_BLOCK_128x128) return FP8Q_ERR_UNSUPPORTED;
   if (K % 128 || N % 128) return FP8Q_ERR_UNSUPPORTED;
   if (((M + 127) / 128) * (N / 128) > 0x7fffffff) return FP8Q_ERR_UNSUPPORTED;
@@ -290,28 +306,30 @@ fp8q_status fp8q_gemm_quantized(const uint8_t* A, const float* sA, fp8q_granular
 }
 
 int64_t fp8q_calibrate_clip_workspace(int64_t n) {
-  if (n <= 0) return -1;
+  if (n <= 0 || n > kMaxClipTokens) return -1;
   int64_t chunk, blocks;
   clip_blocks(n, chunk, blocks);
   return blocks * fp8q::clip_slots(fp8q::kClipMaxL, fp8q::kClipMaxH) * (int64_t)sizeof(double);
 }
 
-fp8q_status fp8q_calibrate_clip(const float* adv, const float* w_tis, const float* pi_sampler, const float* r_bf16,
-                                const float* r_fp8, int64_t n, double l_old, double h_old,
-                                const fp8q_clip_config* config, void* workspace, int64_t workspace_bytes,
-                                fp8q_clip_result* result, struct ihipStream_t* stream) {
-  if (!adv || !w_tis || !pi_sampler || !r_bf16 || !r_fp8 || !config || !workspace || !result) return FP8Q_ERR_INVAL;
+namespace {
+
+// The checks shared by both Calibrated Clipping entry points (all but the
+// workspace's), then the kernel arguments without the partials' address.
+fp8q_status clip_args(const float* adv, const float* w_tis, const float* pi_sampler, const float* r_bf16,
+                      const float* r_fp8, int64_t n, double l_old, double h_old, const fp8q_clip_config* config,
+                      fp8q_clip_result* result, fp8q::ClipArgs& p) {
+  if (!adv || !w_tis || !pi_sampler || !r_bf16 || !r_fp8 || !config || !result) return FP8Q_ERR_INVAL;
   if (n <= 0) return FP8Q_ERR_INVAL;
+  if (n > kMaxClipTokens) return FP8Q_ERR_UNSUPPORTED;
   const fp8q_clip_config c = *config;
   if (!(c.step > 0.0) || !(c.l_max >= c.l_min) || !(c.h_max >= c.h_min)) return FP8Q_ERR_INVAL;
   int nl, nh;
   if (!grid_size(c.l_min, c.l_max, c.step, nl) || !grid_size(c.h_min, c.h_max, c.step, nh)) return FP8Q_ERR_INVAL;
   if (nl > fp8q::kClipMaxL || nh > fp8q::kClipMaxH) return FP8Q_ERR_UNSUPPORTED;
-  if (workspace_bytes < fp8q_calibrate_clip_workspace(n)) return FP8Q_ERR_INVAL;
   if (!aligned(adv, 16) || !aligned(w_tis, 16) || !aligned(pi_sampler, 16) || !aligned(r_bf16, 16) ||
-      !aligned(r_fp8, 16) || !aligned(workspace, 8) || !aligned(result, 8))
+      !aligned(r_fp8, 16) || !aligned(result, 8))
     return FP8Q_ERR_ALIGN;
-  fp8q::ClipArgs p;
   p.adv = adv;
   p.w = w_tis;
   p.pi = pi_sampler;
@@ -333,13 +351,29 @@ fp8q_status fp8q_calibrate_clip(const float* adv, const float* w_tis, const floa
   p.delta_h = c.delta_h;
   p.l_old = l_old;
   p.h_old = h_old;
-  p.partials = static_cast<double*>(workspace);
+  p.partials = nullptr;
   p.result = result;
+  return FP8Q_OK;
+}
+
+}  // namespace
+
+fp8q_status fp8q_calibrate_clip(const float* adv, const float* w_tis, const float* pi_sampler, const float* r_bf16,
+                                const float* r_fp8, int64_t n, double l_old, double h_old,
+                                const fp8q_clip_config* config, void* workspace, int64_t workspace_bytes,
+                                fp8q_clip_result* result, struct ihipStream_t* stream) {
+  fp8q::ClipArgs p;
+  const fp8q_status st = clip_args(adv, w_tis, pi_sampler, r_bf16, r_fp8, n, l_old, h_old, config, result, p);
+  if (st != FP8Q_OK) return st;
+  if (!workspace || workspace_bytes < fp8q_calibrate_clip_workspace(n)) return FP8Q_ERR_INVAL;
+  if (!aligned(workspace, 8)) return FP8Q_ERR_ALIGN;
+  p.partials = static_cast<double*>(workspace);
   return from_hip(fp8q::launch_calibrate_clip(p, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, struct ihipStream_t* stream) {
   if (!x || !codes || n <= 0 || !(scale > 0.0f)) return FP8Q_ERR_INVAL;
+  if (n > ((int64_t)1 << 62)) return FP8Q_ERR_UNSUPPORTED;
   if (!aligned(x, 4)) return FP8Q_ERR_ALIGN;
   return from_hip(fp8q::launch_cast_f32(x, n, scale, false, codes, reinterpret_cast<hipStream_t>(stream)));
 }
@@ -347,6 +381,7 @@ fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes
 fp8q_status fp8q_cast_f32_e5m2(const float* x, int64_t n, float scale, uint8_t* codes,
                                struct ihipStream_t* stream) {
   if (!x || !codes || n <= 0 || !(scale > 0.0f)) return FP8Q_ERR_INVAL;
+  if (n > ((int64_t)1 << 62)) return FP8Q_ERR_UNSUPPORTED;
   if (!aligned(x, 4)) return FP8Q_ERR_ALIGN;
   return from_hip(fp8q::launch_cast_f32(x, n, scale, true, codes, reinterpret_cast<hipStream_t>(stream)));
 }

@@ -385,7 +385,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   // rows x 4 tile columns (one band) on an XCD at a time and then the next
   // band of the same rows, which so starts on the K blocks of A the last one
   // ended with, still in L2.  Every tile shape takes the same direction for
-  // an output element, so a grouped launch sums as a single call would.
+  // an output element, so a grouped launch sums as a single call would (and
+  // so does each sub-problem of a split launch, whose column origins are
+  // multiples of 2048 while ldb < 2^20).
   const bool rev = ((n0 >> 10) & 1) != 0;
   auto kb = [&](int st) { return (rev ? KT - 1 - st : st) * KS + kg; };
   const int mw = (int)m0 + wm, nw = (int)n0 + wn;  // wave's first row / column
@@ -400,8 +402,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   // columns n = nw + 16 j + 4 (lane / 16) + r.  Per K block kt the row
   // scales of A sit at sA[kt * sa_ld + m] (1x128) and the scales of B at
   // sB[(n / 128) * (K / 128) + kt] (128x128) or sB[kt * sb_ld + n] (1x128).
-  // Reads past the scale arrays return zero through the buffer bounds (they
-  // only feed rows or columns that are never stored).
+  // The staged scale vectors of a tile cover whole tiles: entries for rows
+  // past M (columns past N) repeat the last row's (column's) scale, so that
+  // every address stays inside the arrays; they only feed rows or columns
+  // that are never stored.
   const __amdgpu_buffer_rsrc_t rsA = make_rsrc(g.sA, (uint32_t)(g.sa_count * 4));
   const __amdgpu_buffer_rsrc_t rsB = make_rsrc(g.sB, (uint32_t)(g.sb_count * 4));
   const int kblocks = (int)(g.K / 128);
@@ -415,19 +419,25 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   const __amdgpu_buffer_rsrc_t rs_q = q_is_a ? rsA : rsB;
   int q_dst = 0, q_voff = 0x7fffffff, q_ld = 0, q_base = 0;
   auto scale_offsets = [&]() {  // of the tile at (m0, n0)
+    const int last_m = (int)(g.M - 1 - m0), last_n = (int)(g.N - 1 - n0);  // >= 0: the tile is inside C
     if (wave < kQA) {
       q_dst = wave * 256;
-      q_voff = (wave * 64 + lane) * 4;
+      const int r = wave * 64 + lane;
+      q_voff = (r < last_m ? r : last_m) * 4;
       q_ld = (int)g.sa_ld * 4;
       q_base = (int)m0 * 4;
     } else if (wave < kQ) {
       q_dst = kScaleA + (wave - kQA) * 256;
       if (kWeightBlocks) {
-        // the tile's BN / 128 weight blocks, each with K / 128 scales
-        q_voff = lane < (BN + 127) / 128 ? ((int)(n0 / 128) + lane) * kblocks * 4 : 0x7fffffff;
+        // the tile's BN / 128 weight blocks, each with K / 128 scales (the
+        // lanes past them read past the array: zeros through the bounds of
+        // the vector offset)
+        const int nb = (int)(n0 / 128) + (lane < last_n / 128 ? lane : last_n / 128);
+        q_voff = lane < (BN + 127) / 128 ? nb * kblocks * 4 : 0x7fffffff;
         q_ld = 4;
       } else {
-        q_voff = ((wave - kQA) * 64 + lane) * 4;
+        const int c = (wave - kQA) * 64 + lane;
+        q_voff = (c < last_n ? c : last_n) * 4;
         q_ld = (int)g.sb_ld * 4;
         q_base = (int)n0 * 4;
       }
@@ -961,7 +971,13 @@ hipError_t launch_split(const GemmArgs& g, hipStream_t s) {
     const int64_t cstep = ((lim - 1) / c_row_bytes) / 256 * 256;
     if (cstep < mstep) mstep = cstep;
   }
-  if (g.N * g.ldb >= lim) nstep = ((lim - 1) / g.ldb) / 256 * 256;
+  // column steps in whole 2048-column pairs of bands, so that a
+  // sub-problem's tiles take the K direction of their global columns
+  // (odd 1024-column bands walk K backwards)
+  if (g.N * g.ldb >= lim) {
+    const int64_t q = (lim - 1) / g.ldb;
+    nstep = q >= 2048 ? q / 2048 * 2048 : q / 256 * 256;
+  }
   if (mstep > ((int64_t)1 << 28)) mstep = (int64_t)1 << 28;
   if (nstep > ((int64_t)1 << 28)) nstep = (int64_t)1 << 28;
   if (mstep <= 0 || nstep <= 0) return hipErrorInvalidValue;

@@ -91,6 +91,20 @@ def grads(M, N, seed, device="cpu"):
     return normal_bf16((M, N), SIGMA_DY, seed, device)
 
 
+def weights_block_gains(N, K, seed, gain_seed, device="cpu"):
+    """weights() with each 128 x 128 block (of rows and columns) multiplied
+    by its own power of two 2^g, g drawn uniformly from -6 .. 6 with a
+    seeded generator: exact in bf16, and the blocks' scales then differ by
+    up to 2^12 instead of a few percent."""
+    w = weights(N, K, seed, device)
+    gen = torch.Generator()
+    gen.manual_seed(gain_seed)
+    g = torch.randint(-6, 7, ((N + 127) // 128, (K + 127) // 128), generator=gen)
+    gains = torch.pow(2.0, g.to(torch.float32))
+    gains = gains.repeat_interleave(128, 0)[:N].repeat_interleave(128, 1)[:, :K]
+    return (w.to(torch.float32) * gains.to(w.device)).to(torch.bfloat16)
+
+
 def bf16_bits(t):
     """bf16 tensor -> numpy uint16 bit patterns (CPU copy)."""
     return t.detach().cpu().contiguous().view(torch.int16).numpy().view("uint16")

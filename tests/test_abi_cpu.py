@@ -277,6 +277,15 @@ def test_calibrate_clip_workspace_and_rejections(L):
     assert calib(L, res=FAKE + 4) == -3
 
 
+def test_calibrate_clip_batch_limit(L):
+    """Every batch's partials take at most 256 blocks of sums; batches past
+    2^52 tokens are refused."""
+    for n in (1, 4096, 1 << 20, 1 << 40, 1 << 52):
+        assert 0 < L.fp8q_calibrate_clip_workspace(n) <= 212992
+    assert L.fp8q_calibrate_clip_workspace((1 << 52) + 1) == -1
+    assert calib(L, n=(1 << 52) + 1) == -2
+
+
 def test_binding_rejects_short_or_misshapen_buffers():
     """The Python binding checks caller-supplied outputs and scale arrays
     before any call: the kernels read and write exactly the sizes the shapes

@@ -250,6 +250,53 @@ def test_full_32b_backward_operands():
     check(x.cpu(), fp8q.BLOCK_128x1, transposed=True, label="X^T 32B")
 
 
+def _full_operands():
+    """Every quantized operand of the five workloads not covered above, as
+    (label, maker, granularity, transposed); makers draw the same seeded
+    tensors as the GEMM tests of each workload."""
+    a, w, g = synth.activations, synth.weights, synth.grads
+    sf = synth.seed_for
+    B1, B128, R, T = fp8q.BLOCK_1x128, fp8q.BLOCK_128x128, fp8q.ROW, fp8q.TENSOR
+    out = [
+        ("tiny A", lambda: synth.normal_bf16((128, 256), 1.0, sf(1, 0), DEV), T, False),
+        ("tiny B", lambda: synth.normal_bf16((256, 256), 0.02, sf(1, 1), DEV), T, False),
+        ("rowwise down X 16384x12288", lambda: a(16384, 12288, sf(3, 0, 1), sf(3, 3, 1), DEV), R, False),
+        ("rowwise QKV X 16384x4096", lambda: a(16384, 4096, sf(3, 0, 2), sf(3, 3, 2), DEV), R, False),
+        ("rowwise QKV W 6144x4096", lambda: w(6144, 4096, sf(3, 1, 2), DEV), R, False),
+    ]
+    for i, (M, K, N) in enumerate(synth.WORKLOADS["8b_decode_blockwise"]["shapes"]):
+        out.append(("decode X %dx%d" % (M, K), lambda M=M, K=K, i=i: a(M, K, sf(4, 0, i), sf(4, 3, i), DEV), B1, False))
+        out.append(("decode W %dx%d" % (N, K), lambda N=N, K=K, i=i: w(N, K, sf(4, 1, i), DEV), B128, False))
+    for si, proj, k_in, n_out in ((0, "up", 5120, 25600), (3, "down", 25600, 5120)):
+        mk_x = lambda k_in=k_in, si=si: a(16384, k_in, sf(5, 0, si), sf(5, 3, si), DEV)
+        mk_w = lambda k_in=k_in, n_out=n_out, si=si: w(n_out, k_in, sf(5, 1, si), DEV)
+        mk_dy = lambda n_out=n_out, si=si: g(16384, n_out, sf(5, 2, si), DEV)
+        out.append(("32B %s X (fwd)" % proj, mk_x, B1, False))
+        out.append(("32B %s W (fwd)" % proj, mk_w, B128, False))
+        out.append(("32B %s W^T (dgrad)" % proj, mk_w, B128, True))
+        if proj == "down":   # (the up projection's are checked above)
+            out.append(("32B down X^T (wgrad)", mk_x, fp8q.BLOCK_128x1, True))
+            out.append(("32B down dY (dgrad)", mk_dy, B1, False))
+            out.append(("32B down dY^T (wgrad)", mk_dy, fp8q.BLOCK_128x1, True))
+    out.append(("8B W with 128x128 block gains", lambda: synth.weights_block_gains(12288, 4096, sf(2, 1), 77, DEV),
+                B128, False))
+    out.append(("8B W^T with 128x128 block gains", lambda: synth.weights_block_gains(12288, 4096, sf(2, 1), 77, DEV),
+                B128, True))
+    return out
+
+
+@pytest.mark.parametrize("case", _full_operands(), ids=lambda c: c[0])
+def test_full_workload_operands(case):
+    """Byte for byte against the oracle: the remaining operands of the five
+    workloads at full size (both 32B projections' weights plain and
+    transposed, their inputs and output gradients in every layout the
+    forward, dgrad and wgrad GEMMs take, the rowwise and decode operands,
+    the tiny workload's) and a weight whose 128 x 128 blocks carry power-of-
+    two gains from 2^-6 to 2^6."""
+    label, make, g, transposed = case
+    check(make().cpu(), g, transposed, label=label)
+
+
 def test_binding_checks_buffers():
     """Caller-supplied outputs and scale arrays of the wrong shape or too
     few elements are refused by the binding before any kernel runs."""

@@ -72,9 +72,10 @@ def gemm_pow2_vs_oracle(x, w, rows=None, label=""):
     oA, osA = _par.quantize(synth.bf16_bits(x[idx].cpu()), oracle.BLOCK_1x128, pow2=True)
     oB, osB = _par.quantize(synth.bf16_bits(w.cpu()), oracle.BLOCK_128x128, pow2=True)
     ref = _par.gemm_rows(oA, osA, oracle.BLOCK_1x128, oB, osB, oracle.BLOCK_128x128, np.arange(len(rows)))
-    err = _par.rel_err(got, ref)
-    print("  max rel err (row normwise) %.3e" % err, flush=True)
-    assert err <= TOL, err
+    # power-of-two scales enter the instruction: the accumulator carries
+    # the scaled sum through every K block
+    _par.check_gemm(got, ref, oA, osA, oracle.BLOCK_1x128, oB, osB, oracle.BLOCK_128x128, "accumulate",
+                    tol=TOL, label=label)
 
 
 def test_gemm_small_tiles():
@@ -118,3 +119,13 @@ def test_gemm_full_8b_ffn_up():
     x = synth.activations(M, K, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=DEV)
     w = synth.weights(N, K, seed=synth.seed_for(2, 1), device=DEV)
     gemm_pow2_vs_oracle(x, w, _par.sample_rows(M), "8B up fwd")
+
+
+def test_gemm_full_8b_block_gains():
+    """Power-of-two block scales that differ by up to 2^12 between the
+    weight's 128 x 128 blocks (the synthetic weights alone give one scale
+    for nearly every block)."""
+    M, K, N = 16384, 4096, 12288
+    x = synth.activations(M, K, seed=synth.seed_for(2, 0), outlier_seed=synth.seed_for(2, 3), device=DEV)
+    w = synth.weights_block_gains(N, K, seed=synth.seed_for(2, 1), gain_seed=79, device=DEV)
+    gemm_pow2_vs_oracle(x, w, rows=_par.sample_rows(M), label="8B up fwd, block gains")

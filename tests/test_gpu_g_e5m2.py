@@ -137,10 +137,9 @@ def run_formats(a_src, b_src, ga, gb, fa, fb, a_t=False, b_t=False, rows=None, l
     ref = _par.gemm_rows(oA, osA, ga, oB, osB, gb, np.arange(len(rows)),
                          fmtA=oracle.FMT_E5M2 if fa else oracle.FMT_E4M3,
                          fmtB=oracle.FMT_E5M2 if fb else oracle.FMT_E4M3)
-    err = _par.rel_err(got, ref)
-    print("  max rel err (row normwise) %.3e" % err, flush=True)
-    assert err <= TOL, err
-    return err
+    return _par.check_gemm(got, ref, oA, osA, ga, oB, osB, gb, "promote",
+                           fmtA=oracle.FMT_E5M2 if fa else oracle.FMT_E4M3,
+                           fmtB=oracle.FMT_E5M2 if fb else oracle.FMT_E4M3, tol=TOL, label=label)
 
 
 # (tokens, layer input width = dX columns, layer output width = contraction)

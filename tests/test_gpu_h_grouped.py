@@ -42,9 +42,9 @@ def check_group(a_list, w_list, ga, gb, rows=None, label=""):
         oA, osA = _par.quantize(synth.bf16_bits(src.cpu()), ga)
         oB, osB = _par.quantize(synth.bf16_bits(w.cpu()), gb)
         ref = _par.gemm_rows(oA, osA, ga, oB, osB, gb, r if ga == fp8q.TENSOR else np.arange(len(r)))
-        err = _par.rel_err(c.float().cpu().numpy()[r], ref)
-        print("  problem %d max rel err (row normwise) %.3e" % (i, err), flush=True)
-        assert err <= TOL, (i, err)
+        kind = "accumulate" if ga in (fp8q.TENSOR, fp8q.ROW) else "promote"
+        _par.check_gemm(c.float().cpu().numpy()[r], ref, oA[r] if ga == fp8q.TENSOR else oA, osA, ga,
+                        oB, osB, gb, kind, tol=TOL, label="problem %d" % i)
 
 
 @pytest.mark.parametrize("ga,gb", [(fp8q.BLOCK_1x128, fp8q.BLOCK_128x128), (fp8q.ROW, fp8q.ROW),
