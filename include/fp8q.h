@@ -27,8 +27,9 @@
  * rejected call enqueues nothing.  Sizes and leading dimensions above
  * 2^31 - 1 elements (Calibrated Clipping batches above 2^52 tokens, casts
  * above 2^62 values) are FP8Q_ERR_UNSUPPORTED.  Faults inside kernels surface at the
- * caller's next synchronization.  The library holds no mutable global
- * state, so calls from several threads are safe; calls that write the same
+ * caller's next synchronization.  Apart from the one device array of
+ * fp8q_calibrate_clip_noalloc, the library holds no mutable global state,
+ * so calls from several threads are safe; calls that write the same
  * buffers must be ordered by the caller.
  */
 #ifndef FP8Q_H
@@ -325,6 +326,33 @@ fp8q_status fp8q_calibrate_clip(const float *adv, const float *w_tis,
                                 void *workspace, int64_t workspace_bytes,
                                 fp8q_clip_result *result,
                                 struct ihipStream_t *stream);
+
+/*
+ * fp8q_calibrate_clip without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses
+ * that forbid allocation).  Arguments, results and every rule are those of
+ * fp8q_calibrate_clip; the partial sums go to an array of the library's
+ * own instead of a workspace.  This call allocates nothing.
+ *
+ * The array holds FP8Q_CLIP_SCRATCH_BYTES (212992) bytes on each device
+ * the call runs on (the device of `stream`, or the current device for the
+ * null stream), from the first call on that device until the process
+ * ends; that first call looks up its address.  Every batch fits it (a
+ * batch is split into at most 256 blocks of partial sums); a batch whose
+ * partials would not fit is FP8Q_ERR_UNSUPPORTED.  Nothing in it needs to
+ * start cleared: each call writes every partial it reads.  All calls on one
+ * device share the array, so calls that may overlap on one device (on
+ * different streams without ordering between them) race: order them.
+ * A failed address lookup is FP8Q_ERR_HIP.
+ */
+enum { FP8Q_CLIP_SCRATCH_BYTES = 212992 };
+fp8q_status fp8q_calibrate_clip_noalloc(const float *adv, const float *w_tis,
+                                        const float *pi_sampler,
+                                        const float *r_bf16, const float *r_fp8,
+                                        int64_t n, double l_old, double h_old,
+                                        const fp8q_clip_config *config,
+                                        fp8q_clip_result *result,
+                                        struct ihipStream_t *stream);
 
 /*
  * Q_FP8(RN32(x[i] / scale)) for n fp32 values with one explicit scale (Eq.

@@ -26,7 +26,8 @@ _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
            "fp8q_gemm", "fp8q_gemm_grouped", "fp8q_gemm_formats", "fp8q_gemm_pow2", "fp8q_gemm_quantized",
-           "fp8q_calibrate_clip_workspace", "fp8q_calibrate_clip", "fp8q_cast_f32",
+           "fp8q_calibrate_clip_workspace", "fp8q_calibrate_clip", "fp8q_calibrate_clip_noalloc",
+           "fp8q_cast_f32",
            "fp8q_cast_f32_e5m2", "fp8q_status_string")
 
 
@@ -102,6 +103,8 @@ def lib():
         L.fp8q_calibrate_clip.argtypes = [p, p, p, p, p, i64, d, d, ctypes.POINTER(ClipConfig),
                                           p, i64, p, p]
         L.fp8q_calibrate_clip.restype = i32
+        L.fp8q_calibrate_clip_noalloc.argtypes = [p, p, p, p, p, i64, d, d, ctypes.POINTER(ClipConfig), p, p]
+        L.fp8q_calibrate_clip_noalloc.restype = i32
         L.fp8q_cast_f32.argtypes = [p, i64, ctypes.c_float, p, p]
         L.fp8q_cast_f32_e5m2.argtypes = [p, i64, ctypes.c_float, p, p]
         L.fp8q_cast_f32_e5m2.restype = i32
@@ -359,6 +362,29 @@ def calibrate_clip(adv, w_tis, pi_sampler, r_bf16, r_fp8, l_old, h_old, config=N
                                    ctypes.byref(cfg), workspace.data_ptr(), workspace.numel(),
                                    result.data_ptr(), _stream(adv))
     _check(st, "fp8q_calibrate_clip")
+    if not read:
+        return None
+    r = ClipResult.from_buffer_copy(result.cpu().numpy().tobytes())
+    return {name: getattr(r, name) for name, _ in ClipResult._fields_}
+
+
+def calibrate_clip_noalloc(adv, w_tis, pi_sampler, r_bf16, r_fp8, l_old, h_old, config=None,
+                           result=None, read=True):
+    """calibrate_clip() through fp8q_calibrate_clip_noalloc: no workspace,
+    the partial sums go to the library's own device array (calls on one
+    device must not overlap).  `result` and `read` as for calibrate_clip."""
+    ts = (adv, w_tis, pi_sampler, r_bf16, r_fp8)
+    n = adv.numel()
+    for t in ts:
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous() or t.numel() != n:
+            raise ValueError("inputs must be contiguous float32 CUDA tensors of one length")
+    cfg = ClipConfig(**(config or PAPER_CLIP_CONFIG))
+    if result is None:
+        result = torch.empty(ctypes.sizeof(ClipResult), dtype=torch.uint8, device=adv.device)
+    _vector(result, torch.uint8, ctypes.sizeof(ClipResult), "result", adv.device)
+    st = lib().fp8q_calibrate_clip_noalloc(*(t.data_ptr() for t in ts), n, float(l_old), float(h_old),
+                                           ctypes.byref(cfg), result.data_ptr(), _stream(adv))
+    _check(st, "fp8q_calibrate_clip_noalloc")
     if not read:
         return None
     r = ClipResult.from_buffer_copy(result.cpu().numpy().tobytes())

@@ -371,6 +371,23 @@ fp8q_status fp8q_calibrate_clip(const float* adv, const float* w_tis, const floa
   return from_hip(fp8q::launch_calibrate_clip(p, reinterpret_cast<hipStream_t>(stream)));
 }
 
+fp8q_status fp8q_calibrate_clip_noalloc(const float* adv, const float* w_tis, const float* pi_sampler,
+                                        const float* r_bf16, const float* r_fp8, int64_t n, double l_old,
+                                        double h_old, const fp8q_clip_config* config, fp8q_clip_result* result,
+                                        struct ihipStream_t* stream) {
+  fp8q::ClipArgs p;
+  const fp8q_status st = clip_args(adv, w_tis, pi_sampler, r_bf16, r_fp8, n, l_old, h_old, config, result, p);
+  if (st != FP8Q_OK) return st;
+  // the partials of any batch fit (at most kClipMaxBlocks blocks); checked
+  // all the same, before anything is enqueued
+  if (fp8q_calibrate_clip_workspace(n) > fp8q::kClipScratchBytes) return FP8Q_ERR_UNSUPPORTED;
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  double* partials = nullptr;
+  if (fp8q::clip_scratch(s, &partials) != hipSuccess) return FP8Q_ERR_HIP;
+  p.partials = partials;
+  return from_hip(fp8q::launch_calibrate_clip(p, s));
+}
+
 fp8q_status fp8q_cast_f32(const float* x, int64_t n, float scale, uint8_t* codes, struct ihipStream_t* stream) {
   if (!x || !codes || n <= 0 || !(scale > 0.0f)) return FP8Q_ERR_INVAL;
   if (n > ((int64_t)1 << 62)) return FP8Q_ERR_UNSUPPORTED;

@@ -24,6 +24,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "fp8q.h"
 #include "internal.h"
 
@@ -463,6 +465,48 @@ hipError_t launch_calibrate_clip(const ClipArgs& p, hipStream_t s) {
   // threads a block (three waves per SIMD)
   if (p.nl <= 21 && p.nh <= 41) return clip_detail::launch<21, 41, 768>(p, s);
   return clip_detail::launch<kClipMaxL, kClipMaxH, 768>(p, s);
+}
+
+// The partial sums of the allocation-free entry point: room for the most
+// blocks a batch is split into and the largest grids, on every device the
+// library runs on, for the life of the process.  In host code `scratch`
+// only stands in for the symbol: its device address comes from
+// hipGetSymbolAddress, once per device, and only that address is used.
+static __device__ __align__(256) double scratch[kClipScratchBytes / sizeof(double)];
+static_assert(kClipScratchBytes ==
+                  (int64_t)kClipMaxBlocks * clip_detail::Slots<kClipMaxL, kClipMaxH>::kTotal * sizeof(double),
+              "the scratch holds the partials of kClipMaxBlocks blocks at the largest grids");
+
+hipError_t clip_scratch(hipStream_t s, double** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static double* addr[kMaxDevices] = {};
+  int cur = 0, dev = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  dev = cur;
+  if (s) {
+    e = hipStreamGetDevice(s, &dev);
+    if (e != hipSuccess) return e;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    // the lookup runs with the stream's device current (each device holds
+    // its own copy of the array at its own address)
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = static_cast<double*>(p);
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace fp8q

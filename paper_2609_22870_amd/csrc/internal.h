@@ -101,4 +101,11 @@ using ClipResult = fp8q_clip_result;
 int clip_slots(int nl, int nh);
 hipError_t launch_calibrate_clip(const ClipArgs& p, hipStream_t s);
 
+// Bytes of the library's own partial-sum array for fp8q_calibrate_clip_noalloc:
+// kClipMaxBlocks blocks of clip_slots(kClipMaxL, kClipMaxH) float64 sums.
+constexpr int64_t kClipScratchBytes = FP8Q_CLIP_SCRATCH_BYTES;
+// Device address of that array on the device of stream s (the current device
+// for the null stream), looked up on the first call for each device.
+hipError_t clip_scratch(hipStream_t s, double** ptr);
+
 }  // namespace fp8q

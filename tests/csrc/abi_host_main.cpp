@@ -141,17 +141,19 @@ int main() {
   const float* t = fake<const float>();
   fp8q_clip_result* res = fake<fp8q_clip_result>();
   const int64_t ws = fp8q_calibrate_clip_workspace(8863490);
-  EXPECT(ws > 0 && ws <= 212992 ? 0 : 1, 0, 0);
+  EXPECT(ws > 0 && ws <= FP8Q_CLIP_SCRATCH_BYTES ? 0 : 1, 0, 0);
   EXPECT(fp8q_calibrate_clip(t, t, t, t, t, 8863490, 0.6, 1.8, &cfg, C, ws, res, nullptr), FP8Q_OK, 1);
   EXPECT(fp8q_calibrate_clip(t, t, t, t, t, 8863490, 0.6, 1.8, &cfg, C, ws - 8, res, nullptr), FP8Q_ERR_INVAL, 0);
   EXPECT(fp8q_calibrate_clip(t, t, t, t, t, BIG, 0.6, 1.8, &cfg, C, BIG, res, nullptr), FP8Q_ERR_UNSUPPORTED, 0);
   EXPECT(fp8q_calibrate_clip_workspace(BIG), -1, 0);
+  EXPECT(fp8q_calibrate_clip_noalloc(t, t, t, t, t, 8863490, 0.6, 1.8, &cfg, res, nullptr), FP8Q_OK, 1);
+  EXPECT(fp8q_calibrate_clip_noalloc(t, t, t, t, t, BIG, 0.6, 1.8, &cfg, res, nullptr), FP8Q_ERR_UNSUPPORTED, 0);
   fp8q_clip_config bad = cfg;
   bad.step = 0.0;
-  EXPECT(fp8q_calibrate_clip(t, t, t, t, t, 100, 0.6, 1.8, &bad, C, ws, res, nullptr), FP8Q_ERR_INVAL, 0);
+  EXPECT(fp8q_calibrate_clip_noalloc(t, t, t, t, t, 100, 0.6, 1.8, &bad, res, nullptr), FP8Q_ERR_INVAL, 0);
   bad = cfg;
   bad.l_max = 1e300;
-  EXPECT(fp8q_calibrate_clip(t, t, t, t, t, 100, 0.6, 1.8, &bad, C, ws, res, nullptr), FP8Q_ERR_INVAL, 0);
+  EXPECT(fp8q_calibrate_clip_noalloc(t, t, t, t, t, 100, 0.6, 1.8, &bad, res, nullptr), FP8Q_ERR_INVAL, 0);
 
   // casts
   EXPECT(fp8q_cast_f32(t, 1000, 1.0f, codes, nullptr), FP8Q_OK, 1);

@@ -286,6 +286,32 @@ def test_calibrate_clip_batch_limit(L):
     assert calib(L, n=(1 << 52) + 1) == -2
 
 
+def calib_na(L, ptrs=(FAKE,) * 5, n=4096, cfg=None, res=FAKE):
+    import ctypes
+    c = fp8q.ClipConfig(**(cfg or fp8q.PAPER_CLIP_CONFIG))
+    return L.fp8q_calibrate_clip_noalloc(*ptrs, n, 0.6, 1.8, ctypes.byref(c), res, None)
+
+
+def test_calibrate_clip_noalloc_rejections(L):
+    """The allocation-free form takes the same checks, before it looks up
+    its array (no HIP call is made for a rejected call)."""
+    P = fp8q.PAPER_CLIP_CONFIG
+    assert calib_na(L, ptrs=(FAKE,) * 4 + (None,)) == -1
+    assert calib_na(L, res=None) == -1
+    assert calib_na(L, n=0) == -1
+    assert calib_na(L, n=-3) == -1
+    assert calib_na(L, cfg=dict(P, step=-0.02)) == -1
+    assert calib_na(L, cfg=dict(P, h_max=1.1)) == -1
+    assert calib_na(L, cfg=dict(P, l_min=0.42)) == -2
+    assert calib_na(L, ptrs=(FAKE,) * 2 + (FAKE + 8,) + (FAKE,) * 2) == -3
+    assert calib_na(L, res=FAKE + 4) == -3
+    # every batch's partials fit the array: the largest workspace any n needs
+    for n in (1, 4096, 1 << 20, 1 << 40, 1 << 52):
+        assert 0 < L.fp8q_calibrate_clip_workspace(n) <= 212992
+    assert L.fp8q_calibrate_clip_workspace((1 << 52) + 1) == -1
+    assert calib_na(L, n=(1 << 52) + 1) == -2
+
+
 def test_binding_rejects_short_or_misshapen_buffers():
     """The Python binding checks caller-supplied outputs and scale arrays
     before any call: the kernels read and write exactly the sizes the shapes
