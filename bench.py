@@ -449,16 +449,23 @@ def run_sweep(torch, fp8q, synth, dev, warmup=10, reps=30):
 
 
 class Flush:
-    """A 512 MiB device copy (1 GiB of HBM traffic, four times the 256 MB
+    """A read of 1 GiB (a max over a float32 buffer: four times the 256 MB
     last-level cache) run before a repetition, outside its events, so that
-    the kernel timed next reads its operands from HBM."""
+    the kernel timed next reads its operands from HBM.  Read-only: a flush
+    that writes leaves dirty lines whose write-back would land on the timed
+    kernel."""
 
     def __init__(self, torch, dev):
-        self.src = torch.zeros(512 << 20, dtype=torch.uint8, device=dev)
-        self.dst = torch.empty_like(self.src)
+        self.buf = torch.zeros(256 << 20, dtype=torch.float32, device=dev)
+        self.out = torch.empty((), dtype=torch.float32, device=dev)
 
     def __call__(self):
-        self.dst.copy_(self.src)
+        torch_amax(self.buf, self.out)
+
+
+def torch_amax(buf, out):
+    import torch
+    torch.amax(buf, dim=0, out=out)
 
 
 def time_op(torch, stream, f, reps, warmup=10, flush=None):
@@ -478,6 +485,36 @@ def time_op(torch, stream, f, reps, warmup=10, flush=None):
         e.record(stream)
     torch.cuda.synchronize()
     return sorted(s.elapsed_time(e) * 1000.0 for s, e in evs)
+
+
+def time_rotated(torch, stream, fs, reps, warmup=3, flush=None):
+    """Sorted per-call durations in us: each repetition runs every f of fs
+    back to back between two HIP events on the launch stream (after
+    flush(), outside the events), and counts the elapsed time over
+    len(fs).  The fs work on distinct buffers that together exceed the
+    last-level cache, so each call finds its operands in HBM, and the
+    launch gaps of a single timed call are spread over the group."""
+    for _ in range(warmup):
+        if flush is not None:
+            flush()
+        for f in fs:
+            f()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for s, e in evs:
+        if flush is not None:
+            flush()
+        s.record(stream)
+        for f in fs:
+            f()
+        e.record(stream)
+    torch.cuda.synchronize()
+    return sorted(s.elapsed_time(e) * 1000.0 / len(fs) for s, e in evs)
+
+
+def rotation(nbytes, total=768 << 20, most=16):
+    """How many buffer sets of nbytes each make up about `total` bytes (at
+    least 2, at most `most`)."""
+    return int(max(2, min(most, -(-total // max(1, int(nbytes))))))
 
 
 def percentiles(ts):
@@ -520,20 +557,28 @@ def run_config(torch, fp8q, synth, dev, cfg, reps):
 
     def quant(label, x, g, transposed=False, **kw):
         codes, scales = fp8q.quantize(x, g, transposed, **kw)
-        ts = time_op(torch, stream, lambda: fp8q.quantize(x, g, transposed, codes=codes, scales=scales, **kw),
-                     reps, flush=flush)
         rows, cols = x.shape
-        emit("quantize " + label, ts, "hbm", 3.0 * rows * cols + 4.0 * scales.numel(),
-             PEAK_HBM_GBS, {"shape": [rows, cols], "granularity": GRAN_NAMES[g], "transposed": transposed,
-                            "flushed": True})
+        nbytes = 3.0 * rows * cols + 4.0 * scales.numel()
+        sets = [(x, codes, scales)] + [(x.clone(), torch.empty_like(codes), torch.empty_like(scales))
+                                       for _ in range(rotation(nbytes) - 1)]
+        fs = [lambda s=s: fp8q.quantize(s[0], g, transposed, codes=s[1], scales=s[2], **kw) for s in sets]
+        ts = time_rotated(torch, stream, fs, reps, flush=flush)
+        del sets, fs
+        emit("quantize " + label, ts, "hbm", nbytes, PEAK_HBM_GBS,
+             {"shape": [rows, cols], "granularity": GRAN_NAMES[g], "transposed": transposed, "flushed": True})
         return codes, scales
 
     def dual(label, x):
         outs = fp8q.quantize_dual(x)
-        ts = time_op(torch, stream, lambda: fp8q.quantize_dual(x, *outs), reps, flush=flush)
         rows, cols = x.shape
-        emit("quantize_dual " + label, ts, "hbm", 4.0 * rows * cols + 4.0 * (outs[1].numel() + outs[3].numel()),
-             PEAK_HBM_GBS, {"shape": [rows, cols], "granularity": "1x128 + 128x1 transposed", "flushed": True})
+        nbytes = 4.0 * rows * cols + 4.0 * (outs[1].numel() + outs[3].numel())
+        sets = [(x, outs)] + [(x.clone(), tuple(torch.empty_like(o) for o in outs))
+                              for _ in range(rotation(nbytes) - 1)]
+        fs = [lambda s=s: fp8q.quantize_dual(s[0], *s[1]) for s in sets]
+        ts = time_rotated(torch, stream, fs, reps, flush=flush)
+        del sets, fs
+        emit("quantize_dual " + label, ts, "hbm", nbytes, PEAK_HBM_GBS,
+             {"shape": [rows, cols], "granularity": "1x128 + 128x1 transposed", "flushed": True})
         return outs
 
     def gemm(label, a, sa, ga, b, sb, gb, hbm=False):
@@ -546,7 +591,12 @@ def run_config(torch, fp8q, synth, dev, cfg, reps):
         extra = {"shape_mkn": [M, K, N], "scaling": "%s x %s" % (GRAN_NAMES[ga], GRAN_NAMES[gb]),
                  "flushed": hbm}
         if hbm:
-            ts = time_op(torch, stream, f, reps, flush=flush)
+            # distinct copies of both operands (and outputs) for every call
+            sets = [(a, b, out)] + [(a.clone(), b.clone(), torch.empty_like(out))
+                                    for _ in range(rotation(nbytes) - 1)]
+            fs = [lambda s=s: fp8q.gemm(s[0], sa, ga, s[1], sb, gb, out=s[2]) for s in sets]
+            ts = time_rotated(torch, stream, fs, reps, flush=flush)
+            del sets, fs
             warm = percentiles(time_op(torch, stream, f, reps))[1]
             extra["tflops_at_p50"] = round(flops / (percentiles(ts)[1] * 1e-6) / 1e12, 1)
             extra["us_p50_back_to_back"] = round(warm, 2)
@@ -716,14 +766,19 @@ def main():
         "timed_wall_s": round(wall, 3),
         "settle": {"seconds": args.settle_s, "untimed_steps": settle_steps},
     }
-    # the quantizers alone with the last-level cache flushed before each
-    # repetition (their in-step figures above may find part of their input
-    # there): median over 50
+    # the quantizers alone, cold: each repetition quantizes distinct copies
+    # of the input (together over the last-level cache) after a flush, so
+    # that no operand comes from the caches (their in-step figures above may
+    # find part of their input there): median over 50
     flush = Flush(torch, dev)
-    tqx = percentiles(time_op(torch, stream, lambda: fp8q.quantize(x, fp8q.BLOCK_1x128, codes=xq, scales=sx),
-                              50, flush=flush))[1]
-    tqw = percentiles(time_op(torch, stream, lambda: fp8q.quantize(w, fp8q.BLOCK_128x128, codes=wq, scales=sw),
-                              50, flush=flush))[1]
+
+    def rotated(src, g, codes, scales, nbytes):
+        sets = [(src, codes, scales)] + [(src.clone(), torch.empty_like(codes), torch.empty_like(scales))
+                                         for _ in range(rotation(nbytes) - 1)]
+        fs = [lambda s=s: fp8q.quantize(s[0], g, codes=s[1], scales=s[2]) for s in sets]
+        return percentiles(time_rotated(torch, stream, fs, 50, flush=flush))[1]
+    tqx = rotated(x, fp8q.BLOCK_1x128, xq, sx, qx_bytes)
+    tqw = rotated(w, fp8q.BLOCK_128x128, wq, sw, qw_bytes)
     del flush
     out["quantize_flushed"] = {
         "x_1x128_us": round(tqx, 2), "x_1x128_gbs": round(qx_bytes / (tqx * 1e-6) / 1e9, 1),

@@ -52,6 +52,21 @@ def test_paper_batch():
     compare(b, 0.6, 1.8, label="paper batch")
 
 
+@pytest.mark.parametrize("prompts,ratio_sigma,fp8_sigma,seed", [(256, 0.12, 0.06, 5101), (64, 0.2, 0.1, 5102),
+                                                                 (64, 0.12, 0.03, 5103)])
+def test_lower_search_in_the_body(prompts, ratio_sigma, fp8_sigma, seed):
+    """BF16 ratios spread widely enough that a few percent or more of the
+    negative-advantage tokens sit at or below c_low_ref = 0.8 (the BF16
+    importance ratios of off-policy batches), so that stage 1 of Alg. 1
+    matches counts in the body of the distribution, not in its far tail,
+    and L* lands inside the grid; the first batch is of the paper's size."""
+    b = synth.rl_batch(prompts, 8, seed=seed, ratio_sigma=ratio_sigma, fp8_sigma=fp8_sigma)
+    got = compare(b, 0.6, 1.8, label="ratio sigma %g, fp8 sigma %g" % (ratio_sigma, fp8_sigma))
+    print("  alpha_low %.4f" % got["alpha_low"], flush=True)
+    assert 0.01 <= got["alpha_low"] <= 0.2
+    assert 0.5 < got["l_star"] < 0.9
+
+
 @pytest.mark.parametrize("seed,fp8_sigma,l_old,h_old", [(11, 0.03, 0.66, 1.5), (12, 0.1, 0.72, 1.3),
                                                         (13, 0.2, 0.55, 1.95)])
 def test_smaller_batches(seed, fp8_sigma, l_old, h_old):
