@@ -19,6 +19,10 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-I", INCLUDE, "-I", CSRC,
 ]
+# Per-source additions.  GEMM: matrix-instruction results in ordinary VGPRs
+# (the compiler otherwise puts the 128 x 128 and 64 x 64 tiles' partials in
+# AGPRs, and every promotion FMA then waits for a v_accvgpr_read copy).
+EXTRA = {"gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def check_no_scratch(src, remarks):
@@ -42,7 +46,7 @@ def build():
 
     def compile_one(src):
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        cmd = [HIPCC] + FLAGS + ["-Rpass-analysis=kernel-resource-usage", "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC] + FLAGS + EXTRA.get(src, []) + ["-Rpass-analysis=kernel-resource-usage", "-c", os.path.join(CSRC, src), "-o", obj]
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError("hipcc failed for %s:\n%s" % (src, r.stderr))
