@@ -60,7 +60,7 @@ def parse():
 
 # Kernel sources whose change invalidates recorded HBM counters.
 GEMM_SOURCES = ["paper_2609_22870_amd/csrc/gemm.hip", "paper_2609_22870_amd/csrc/device_common.h",
-                "paper_2609_22870_amd/csrc/internal.h"]
+                "paper_2609_22870_amd/csrc/internal.h", "paper_2609_22870_amd/_build.py"]
 
 
 def sources_digest(paths):

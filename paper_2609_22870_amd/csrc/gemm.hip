@@ -362,10 +362,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   constexpr int kScaleStage = kScaleA + kScaleB;
   // LDS ring of kStages operand stages (and their scale vectors): the loads
   // of stage kt + kStages - 1 go out during step kt.  The 256 x 256 tile
-  // fits two 64 KB stages; 128 x 128 keeps two (more would cost it its
-  // second workgroup per CU); the 64 x 64 tile of skinny problems, whose
-  // steps are short next to the load latency, keeps four.
-  constexpr int kStages = BM >= 128 ? 2 : 4;
+  // fits two 64 KB stages; 128 x 128 with four waves of 64 x 64 keeps two
+  // (more would cost it its second workgroup per CU); the tiles of skinny
+  // problems, whose steps are short next to the load latency, keep four:
+  // 64 x 64, and 128 x 128 with eight waves of 32 x 64 (one workgroup per
+  // CU).
+  constexpr int kStages = (BM >= 128 && WM >= 64) ? 2 : 4;
   static_assert(KS == 1 || (kStages > 2 && !QOUT), "K groups: the 64 x 64 tile");
   constexpr int kGroupBytes = kStages * kStage + kStages * kScaleStage;
   __shared__ __attribute__((aligned(1024))) uint8_t lds_all[KS * kGroupBytes + KS * kWaves * 256];
@@ -938,9 +940,13 @@ inline bool k_groups(const GemmArgs& g) {
 
 // 256 x 256 tiles (8 waves of 128 x 64) when they fill the chip at least
 // twice over; else 128 x 128 tiles (4 waves of 64 x 64) when they fill it
-// once; else 64 x 64 tiles (4 waves of 32 x 32), for skinny problems such as
-// a decode step, whose time goes into streaming the weights.  Quantized
-// output needs whole 128-column units in a tile: 256 or 128 tiles only.
+// once; else, for skinny problems such as a decode step, whose time goes
+// into streaming the weights: 64 x 64 tiles with two K groups when those
+// fit (k_groups), 128 x 128 tiles of 8 waves of 32 x 64 with a four-stage
+// ring (one workgroup per CU) when there are 128 to 255 of them, and 64 x 64
+// tiles (4 waves of 32 x 32) below that.  Every choice but the K groups sums
+// an output's K blocks in the same order.  Quantized output needs whole
+// 128-column units in a tile: 256 or 128 tiles only.
 template <int PAIR, bool QOUT, int FMT>
 hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
   const int64_t big_tiles = ((g.M + 255) / 256) * ((g.N + 255) / 256);
@@ -953,6 +959,7 @@ hipError_t launch_pair(const GemmArgs& g, hipStream_t s) {
   } else {
     if (mid_tiles >= 256) return launch_tiles<PAIR, 128, 128, 64, 64, QOUT, FMT>(g, s);
     if (k_groups(g)) return launch_tiles<PAIR, 64, 64, 32, 32, QOUT, FMT, 2>(g, s);
+    if (mid_tiles >= 128) return launch_tiles<PAIR, 128, 128, 32, 64, QOUT, FMT>(g, s);
     return launch_tiles<PAIR, 64, 64, 32, 32, QOUT, FMT>(g, s);
   }
 }
@@ -1027,6 +1034,11 @@ FP8Q_GEMM_KERNEL(kPairRow, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairBlock, 256, 256, 128, 64)
 FP8Q_GEMM_KERNEL(kPairBlock, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairBlockK, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL(kPairTensor, 128, 128, 32, 64)
+FP8Q_GEMM_KERNEL(kPairRow, 128, 128, 32, 64)
+FP8Q_GEMM_KERNEL(kPairBlock, 128, 128, 32, 64)
+FP8Q_GEMM_KERNEL(kPairBlockK, 128, 128, 32, 64)
+FP8Q_GEMM_KERNEL(kPairBlockE8, 128, 128, 32, 64)
 FP8Q_GEMM_KERNEL(kPairTensor, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairRow, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL(kPairBlock, 64, 64, 32, 32)
@@ -1036,6 +1048,8 @@ FP8Q_GEMM_KERNEL(kPairBlockE8, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL(kPairBlockE8, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL_FMT(kPairBlock, 256, 256, 128, 64)
 FP8Q_GEMM_KERNEL_FMT(kPairBlock, 128, 128, 64, 64)
+FP8Q_GEMM_KERNEL_FMT(kPairBlock, 128, 128, 32, 64)
+FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 128, 128, 32, 64)
 FP8Q_GEMM_KERNEL_FMT(kPairBlock, 64, 64, 32, 32)
 FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 128, 128, 64, 64)
 FP8Q_GEMM_KERNEL_FMT(kPairBlockK, 64, 64, 32, 32)

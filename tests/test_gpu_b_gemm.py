@@ -102,6 +102,18 @@ def test_small_all_pairs(pair):
 
 
 @pytest.mark.parametrize("pair", list(PAIRS))
+def test_small_all_pairs_eight_wave_tiles(pair):
+    """Between 128 and 255 tiles of 128 x 128 (here 3 x 48, the last tile
+    row ragged): the eight-wave 128 x 128 kernel with four stages, one
+    workgroup per CU (the 8B decode up-projection's path)."""
+    ga, gb = PAIRS[pair]
+    M, K, N = 272, 640, 6144
+    a = synth.activations(M, K, seed=181, outlier_seed=182, device=DEV)
+    b = synth.weights(N, K, seed=183, device=DEV)
+    run_pair(a, b, ga, gb, label=pair + " eight-wave tiles")
+
+
+@pytest.mark.parametrize("pair", list(PAIRS))
 def test_small_all_pairs_k_groups(pair):
     """Eight K blocks on few 64 x 64 tiles: the kernel splits the K blocks
     over two groups of waves and sums their partial tiles (ragged M and,

@@ -15,7 +15,8 @@ codes; they and the scales are inputs, so no FP8 quantization is involved
 
 Shapes are chosen to reach each launch path: 256 x 256 tiles (at least 512
 of them; N = 4096 spans two odd 1024-column bands, which walk K backwards),
-128 x 128 tiles, 64 x 64 tiles with two K groups (an even number of K
+128 x 128 tiles of four waves (at least 256 of them) and of eight waves
+(128 to 255 of them), 64 x 64 tiles with two K groups (an even number of K
 blocks on at most 256 tiles) and with one, and problems split into
 sub-launches because an operand spans 2 GiB (along N, and along M).  The
 scales vary per row, column and block (no two neighbouring blocks alike by
@@ -141,6 +142,7 @@ PAIRS = {
 SHAPES = {
     "256x256 tiles": (8192 + 96, 4096, 4096),     # 33 x 16 = 528 big tiles, ragged last tile row
     "128x128 tiles": (4096 + 32, 1024, 1024),     # 33 x 8 = 264 mid tiles, 68 big ones
+    "128x128 eight-wave tiles": (256 + 32, 6144, 6144),  # 3 x 48 = 144 mid tiles, 4 K bands
     "64x64 two K groups": (160, 512, 512),        # 3 x 8 tiles, 4 K blocks
     "64x64 one K group": (160, 384, 384),         # 3 K blocks
 }
@@ -204,7 +206,8 @@ def test_identity_pow2_gemm(shape):
 
 @pytest.mark.parametrize("formats", [fp8q.A_E5M2, fp8q.B_E5M2, fp8q.A_E5M2 | fp8q.B_E5M2])
 @pytest.mark.parametrize("pair", ["block", "blockk"])
-@pytest.mark.parametrize("shape", ["256x256 tiles", "128x128 tiles", "64x64 two K groups"])
+@pytest.mark.parametrize("shape", ["256x256 tiles", "128x128 tiles", "128x128 eight-wave tiles",
+                                   "64x64 two K groups"])
 def test_identity_e5m2_formats(pair, formats, shape):
     ga, gb = PAIRS[pair]
     M, K, N = SHAPES[shape]

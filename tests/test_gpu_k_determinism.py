@@ -1,7 +1,7 @@
 """Two runs of every kernel form give the same bytes (the outputs of a
 scaled GEMM are not unique within its tolerance, so run-to-run equality is
-asserted on its own): every GEMM launch path (256 x 256, 128 x 128 and
-64 x 64 tiles, the latter with and without two K groups) for every scaling
+asserted on its own): every GEMM launch path (256 x 256 tiles, 128 x 128 tiles of
+four and of eight waves, 64 x 64 tiles with and without two K groups) for every scaling
 pair, the power-of-two and E5M2 forms, the grouped GEMM and the GEMM with
 quantized output; every quantizer granularity plain and transposed
 (including the three-kernel tensor, column and transposed row passes), the
@@ -26,6 +26,7 @@ PAIRS = {
 SHAPES = {
     "256x256 tiles": (8192 + 96, 4096, 4096),
     "128x128 tiles": (4096 + 32, 1024, 1024),
+    "128x128 eight-wave tiles": (256 + 32, 2048, 6144),
     "64x64 two K groups": (160, 512, 512),
     "64x64 one K group": (160, 384, 384),
 }
