@@ -170,8 +170,10 @@ __device__ __forceinline__ uint32_t lds_addr(const uint8_t* p) {
 // sources: the destination is early-clobber against `busy` and `busy2`,
 // fragments of MFMAs possibly in flight or still to be issued (so it never
 // takes those registers), and the
-// address depends on `after`, a VALU result computed from the output of the
-// last MFMA whose source registers may be reused (so that MFMA is done).
+// reads take `after` as an input, a VALU result computed from the output of
+// the last MFMA whose source registers may be reused (so that MFMA is done
+// before they issue).  (Making the addresses themselves depend on it, by an
+// empty asm that rewrites them, cost two register copies per read.)
 //
 // Fragment rows come in strips of 16 (row = strip base + lane % 16), so the
 // swizzle term chunk_swizzle(row) depends on the lane only: the two chunk
@@ -190,11 +192,10 @@ __device__ __forceinline__ FragAddr frag_addr(const uint8_t* lds_tile_strip0) {
 
 template <int IMM>
 __device__ __forceinline__ v8i read_frag(FragAddr a, const v8i& busy, const v8i& busy2, float after) {
-  asm volatile("" : "+v"(a.lo), "+v"(a.hi) : "v"(after));
   uint4 lo, hi;
   asm volatile("ds_read_b128 %0, %2 offset:%4\n\tds_read_b128 %1, %3 offset:%4"
                : "=&v"(lo), "=&v"(hi)
-               : "v"(a.lo), "v"(a.hi), "i"(IMM), "v"(busy), "v"(busy2));
+               : "v"(a.lo), "v"(a.hi), "i"(IMM), "v"(busy), "v"(busy2), "v"(after));
   v8i f;
   f[0] = (int)lo.x; f[1] = (int)lo.y; f[2] = (int)lo.z; f[3] = (int)lo.w;
   f[4] = (int)hi.x; f[5] = (int)hi.y; f[6] = (int)hi.z; f[7] = (int)hi.w;
