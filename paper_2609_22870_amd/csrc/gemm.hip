@@ -6,13 +6,13 @@
 // both the depth of one v_mfma_f32_16x16x128_f8f6f4 and the length of one
 // scale block, so a blockwise step is one MFMA per 16 x 16 tile into a
 // zeroed partial, then one FMA per accumulator that adds S_A * S_B * P.
-// Three shapes are built: 256 x 256 tiles with eight waves of 128 x 64 (the
+// Four shapes are built: 256 x 256 tiles with eight waves of 128 x 64 (the
 // large-problem kernel: 64 FP8 bytes of LDS traffic per MFMA instead of
 // 128), 128 x 128 tiles with four waves of 64 x 64 (small grids, and the
 // (1x128, 1x128) pair whose per-column B scales need more registers), and
-// 64 x 64 tiles with four waves of 32 x 32 for skinny problems such as a
-// decode step, where a few tiles split their K blocks over two groups of
-// waves.
+// for skinny problems such as a decode step, 128 x 128 tiles with eight
+// waves of 32 x 64 and 64 x 64 tiles with four waves of 32 x 32, where a
+// few tiles split their K blocks over two groups of waves.
 //
 // Operand tiles (rows x 128 bytes of K) go global -> LDS with the
 // direct-to-LDS 16-byte buffer loads of gfx950 (no VGPR staging), in a ring
