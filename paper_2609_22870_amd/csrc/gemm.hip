@@ -260,23 +260,35 @@ __device__ __forceinline__ int xcd_order(int total, int b) {
   return xcd * per + (xcd < extra ? xcd : extra) + (b >> 3);
 }
 
-// Tile (tm, tn) at position id of a problem's raster.
+// Tile (tm, tn) at position id of a problem's raster.  A group of kGroupM
+// tile rows streams the whole B operand past the L2s once per group, and A
+// only once in all; when the two operands together overflow the 256 MB
+// last-level cache, those repeated passes over B come from HBM, so if B is
+// the larger operand the raster walks groups of kGroupM tile columns
+// instead (the 32B up-projection's wgrad: A 84 MB, B 419 MB).  The mapping
+// decides only which workgroup computes which tile: each output element's
+// K order is fixed by its column.
+constexpr int64_t kLastLevelCache = 256ll << 20;
 template <int BM, int BN>
-__device__ __forceinline__ void raster(int64_t M, int64_t N, int id, int& tm, int& tn) {
+__device__ __forceinline__ void raster(int64_t M, int64_t N, int64_t K, int id, int& tm, int& tn) {
   const int tiles_m = (int)((M + BM - 1) / BM), tiles_n = (int)((N + BN - 1) / BN);
-  const int per_group = kGroupM * tiles_n;
+  const bool col_groups = N > M && tiles_m > kGroupM && (M + N) * K > kLastLevelCache;
+  const int grouped = col_groups ? tiles_n : tiles_m;  // tiles across the groups
+  const int walked = col_groups ? tiles_m : tiles_n;   // tiles along one group
+  const int per_group = kGroupM * walked;
   const int group = id / per_group;
-  const int first_m = group * kGroupM;
-  const int gsize = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
+  const int first = group * kGroupM;
+  const int gsize = (grouped - first) < kGroupM ? (grouped - first) : kGroupM;
   const int in_group = id - group * per_group;
-  tm = first_m + in_group % gsize;
-  tn = in_group / gsize;
+  const int across = first + in_group % gsize, along = in_group / gsize;
+  tm = col_groups ? along : across;
+  tn = col_groups ? across : along;
 }
 
 template <int BM, int BN>
-__device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int b, int& tm, int& tn) {
+__device__ __forceinline__ void tile_coords(int64_t M, int64_t N, int64_t K, int b, int& tm, int& tn) {
   const int total = (int)((M + BM - 1) / BM) * (int)((N + BN - 1) / BN);
-  raster<BM, BN>(M, N, xcd_order(total, b), tm, tn);
+  raster<BM, BN>(M, N, K, xcd_order(total, b), tm, tn);
 }
 
 // Quantized output: the tile's bf16 C, staged in LDS (row m at byte m *
@@ -384,8 +396,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   const int wm = (wave / kWavesN) * WM, wn = (wave % kWavesN) * WN;
   const int KT = (int)(g.K / kBK) / KS;  // steps of this group (KS divides K / 128)
   // K block of the group's step st.  Tiles whose first column lies in an
-  // odd 1024-column band walk K backwards: the 256 x 256 raster runs 8 tile
-  // rows x 4 tile columns (one band) on an XCD at a time and then the next
+  // odd 1024-column band walk K backwards: the 256 x 256 row-group raster
+  // runs 8 tile rows x 4 tile columns (one band) on an XCD at a time and then the next
   // band of the same rows, which so starts on the K blocks of A the last one
   // ended with, still in L2.  Every tile shape takes the same direction for
   // an output element, so a grouped launch sums as a single call would (and
@@ -902,7 +914,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
 template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT, int KS = 1>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64 * KS) void gemm_kernel(GemmArgs g) {
   int tm, tn;
-  tile_coords<BM, BN>(g.M, g.N, blockIdx.x, tm, tn);
+  tile_coords<BM, BN>(g.M, g.N, g.K, blockIdx.x, tm, tn);
   gemm_tile<PAIR, BM, BN, WM, WN, QOUT, FMT, KS>(g, tm, tn);
 }
 
@@ -917,7 +929,7 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64 * KS) void gemm_grouped_
   int p = 0;
   for (int i = 1; i < gs.count; ++i) p += id >= gs.tile_start[i] ? 1 : 0;
   int tm, tn;
-  raster<BM, BN>(gs.prob[p].M, gs.prob[p].N, id - gs.tile_start[p], tm, tn);
+  raster<BM, BN>(gs.prob[p].M, gs.prob[p].N, gs.prob[p].K, id - gs.tile_start[p], tm, tn);
   gemm_tile<PAIR, BM, BN, WM, WN, false, 0, KS>(gs.prob[p], tm, tn);
 }
 
