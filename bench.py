@@ -581,11 +581,18 @@ def run_config(torch, fp8q, synth, dev, cfg, reps):
              {"shape": [rows, cols], "granularity": "1x128 + 128x1 transposed", "flushed": True})
         return outs
 
-    def gemm(label, a, sa, ga, b, sb, gb, hbm=False):
+    def gemm(label, a, sa, ga, b, sb, gb, hbm=False, splitk=False):
+        """splitk: fp8q_gemm_splitk (one zero-filled workspace shared by
+        the calls, which run in order on one stream) instead of fp8q_gemm."""
         M, K = a.shape
         N = b.shape[0]
         out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
-        f = lambda: fp8q.gemm(a, sa, ga, b, sb, gb, out=out)
+        if splitk:
+            ws = torch.zeros(max(fp8q.gemm_splitk_workspace(M, N, K), 16), dtype=torch.uint8, device=dev)
+            call = lambda a_, b_, o_: fp8q.gemm_splitk(a_, sa, ga, b_, sb, gb, out=o_, workspace=ws)
+        else:
+            call = lambda a_, b_, o_: fp8q.gemm(a_, sa, ga, b_, sb, gb, out=o_)
+        f = lambda: call(a, b, out)
         flops = 2.0 * M * N * K
         nbytes = 1.0 * M * K + 1.0 * N * K + 2.0 * M * N + 4.0 * (sa.numel() + sb.numel())
         extra = {"shape_mkn": [M, K, N], "scaling": "%s x %s" % (GRAN_NAMES[ga], GRAN_NAMES[gb]),
@@ -594,13 +601,13 @@ def run_config(torch, fp8q, synth, dev, cfg, reps):
             # distinct copies of both operands (and outputs) for every call
             sets = [(a, b, out)] + [(a.clone(), b.clone(), torch.empty_like(out))
                                     for _ in range(rotation(nbytes) - 1)]
-            fs = [lambda s=s: fp8q.gemm(s[0], sa, ga, s[1], sb, gb, out=s[2]) for s in sets]
+            fs = [lambda s=s: call(s[0], s[1], s[2]) for s in sets]
             ts = time_rotated(torch, stream, fs, reps, flush=flush)
             del sets, fs
             warm = percentiles(time_op(torch, stream, f, reps))[1]
             extra["tflops_at_p50"] = round(flops / (percentiles(ts)[1] * 1e-6) / 1e12, 1)
             extra["us_p50_back_to_back"] = round(warm, 2)
-            emit("gemm " + label, ts, "hbm", nbytes, PEAK_HBM_GBS, extra)
+            emit(("gemm_splitk " if splitk else "gemm ") + label, ts, "hbm", nbytes, PEAK_HBM_GBS, extra)
         elif cfg == 1:
             emit("gemm " + label, time_op(torch, stream, f, reps), "launch", flops, None, extra)
         else:
@@ -632,6 +639,8 @@ def run_config(torch, fp8q, synth, dev, cfg, reps):
             X, sX = quant("X " + tag, x, gx)
             W, sW = quant("W " + tag, w, gw)
             gemm(tag, X, sX, gx, W, sW, gw, hbm=(cfg == 4))
+            if cfg == 4 and fp8q.gemm_splitk_workspace(M, N, K) > 0:
+                gemm(tag, X, sX, gx, W, sW, gw, hbm=True, splitk=True)
             del x, w, X, sX, W, sW
     else:
         T = 16384

@@ -264,6 +264,42 @@ fp8q_status fp8q_gemm_quantized(const uint8_t *A, const float *sA,
                                 struct ihipStream_t *stream);
 
 /*
+ * Bytes of workspace fp8q_gemm_splitk needs for an M x N x K problem (0 when
+ * that call does not split K and is fp8q_gemm); -1 for a size <= 0 or
+ * above 2^31 - 1.
+ */
+int64_t fp8q_gemm_splitk_workspace(int64_t M, int64_t N, int64_t K);
+
+/*
+ * fp8q_gemm for skinny problems such as a decode step of the FP8 rollout
+ * (Sec. 2.3, Sec. 5: a few hundred rows of activations against a full
+ * weight), where
+ * the 128 x 128 tiles of C are too few to give every CU one (fewer than
+ * 128).  The K blocks of each tile are split over S workgroups (S a power
+ * of two up to 8, S x tiles <= 256, at least four K blocks each), so that
+ * each CU streams 1/S of the tile's operand rows; the S fp32 partial tiles
+ * are added in a fixed order, then rounded to bf16 once.  The product,
+ * pairs, layouts, shape and alignment rules are those of fp8q_gemm, and
+ * the result is the same on every run; its K sum is grouped differently
+ * from fp8q_gemm's, so the last bits of an output can differ.  Problems
+ * with 128 or more tiles, or whose operands span 2 GiB, are not split:
+ * then the call is fp8q_gemm and needs no workspace.
+ * workspace: device memory of at least fp8q_gemm_splitk_workspace(M, N, K)
+ * bytes (workspace_bytes), 16-byte aligned, ZERO-FILLED before its first
+ * use; it holds per-tile arrival counters, which every call leaves at
+ * zero, and the partial tiles.  Calls that share a workspace must not
+ * overlap (issue them on one stream).  Errors: those of fp8q_gemm; a null
+ * or short workspace when the call splits -> INVAL, misaligned -> ALIGN.
+ */
+fp8q_status fp8q_gemm_splitk(const uint8_t *A, const float *sA,
+                             fp8q_granularity gA, int64_t lda,
+                             const uint8_t *B, const float *sB,
+                             fp8q_granularity gB, int64_t ldb, int64_t M,
+                             int64_t N, int64_t K, void *C, int64_t ldc,
+                             void *workspace, int64_t workspace_bytes,
+                             struct ihipStream_t *stream);
+
+/*
  * Calibrated Clipping (Sec. 4, Alg. 1, Eq. 5): new lower and upper PPO
  * clipping bounds for FP8 training from one batch of n tokens.
  *

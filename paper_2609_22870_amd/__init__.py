@@ -26,6 +26,7 @@ _STATUS = {0: "FP8Q_OK", -1: "FP8Q_ERR_INVAL", -2: "FP8Q_ERR_UNSUPPORTED",
 # the entry points of include/fp8q.h
 EXPORTS = ("fp8q_scales_count", "fp8q_quantize", "fp8q_quantize_dual",
            "fp8q_gemm", "fp8q_gemm_grouped", "fp8q_gemm_formats", "fp8q_gemm_pow2", "fp8q_gemm_quantized",
+           "fp8q_gemm_splitk_workspace", "fp8q_gemm_splitk",
            "fp8q_calibrate_clip_workspace", "fp8q_calibrate_clip", "fp8q_calibrate_clip_noalloc",
            "fp8q_cast_f32",
            "fp8q_cast_f32_e5m2", "fp8q_status_string")
@@ -97,6 +98,11 @@ def lib():
         L.fp8q_gemm_quantized.argtypes = [p, p, i32, i64, p, p, i32, i64, i64,
                                           i64, i64, p, i64, p, p]
         L.fp8q_gemm_quantized.restype = i32
+        L.fp8q_gemm_splitk_workspace.argtypes = [i64, i64, i64]
+        L.fp8q_gemm_splitk_workspace.restype = i64
+        L.fp8q_gemm_splitk.argtypes = [p, p, i32, i64, p, p, i32, i64, i64, i64, i64,
+                                       p, i64, p, i64, p]
+        L.fp8q_gemm_splitk.restype = i32
         L.fp8q_calibrate_clip_workspace.argtypes = [i64]
         L.fp8q_calibrate_clip_workspace.restype = i64
         d = ctypes.c_double
@@ -254,6 +260,37 @@ def gemm(a, sa, ga, b, sb, gb, out=None):
                          b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
                          out.data_ptr(), _ld(out), _stream(a))
     _check(st, "fp8q_gemm")
+    return out
+
+
+def gemm_splitk_workspace(M, N, K):
+    """Bytes of workspace gemm_splitk needs for an M x N x K problem (0 when
+    it does not split K)."""
+    need = lib().fp8q_gemm_splitk_workspace(M, N, K)
+    if need < 0:
+        raise ValueError("invalid GEMM size")
+    return need
+
+
+def gemm_splitk(a, sa, ga, b, sb, gb, out=None, workspace=None):
+    """gemm for skinny problems with each output tile's K blocks split over
+    several workgroups (fp8q_gemm_splitk).  workspace: a uint8 CUDA tensor
+    of at least gemm_splitk_workspace(M, N, K) bytes, zero-filled before its
+    first use (a new zero-filled one when None); calls sharing it must be
+    ordered (one stream)."""
+    M, N, K = _operands(a, sa, ga, b, sb, gb)
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    _matrix(out, torch.bfloat16, "out", (M, N), a.device)
+    need = gemm_splitk_workspace(M, N, K)
+    if workspace is None:
+        workspace = torch.zeros(max(need, 16), dtype=torch.uint8, device=a.device)
+    _vector(workspace, torch.uint8, need, "workspace", a.device)
+    st = lib().fp8q_gemm_splitk(a.data_ptr(), sa.data_ptr(), ga, _ld(a),
+                                b.data_ptr(), sb.data_ptr(), gb, _ld(b), M, N, K,
+                                out.data_ptr(), _ld(out), workspace.data_ptr(),
+                                workspace.numel(), _stream(a))
+    _check(st, "fp8q_gemm_splitk")
     return out
 
 

@@ -6,6 +6,36 @@
 #include "fp8q.h"
 #include "internal.h"
 
+namespace fp8q {
+
+// Split-K applies where the tiled kernels leave CUs without a 128 x 128
+// tile (fewer than 128 tiles: a decode step's down-projection, 256 x 4096
+// outputs, has 64): the largest power of two S <= 8 with at most one
+// workgroup per CU (tiles x S <= 256), S dividing the K blocks and at least
+// four K blocks per split.  Problems that launch_split would cut into
+// sub-problems (2 GiB operand spans) are not split.
+int gemm_splitk_splits(int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc) {
+  const int64_t lim = (int64_t)1 << 31;
+  if (M <= 0 || N <= 0 || K <= 0 || K % 128) return 1;
+  if (M * lda >= lim || N * ldb >= lim || M * 2 * ldc >= lim) return 1;
+  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128), kblocks = K / 128;
+  if (tiles >= 128) return 1;
+  int best = 1;
+  for (int sp = 2; sp <= 8; sp *= 2)
+    if (tiles * sp <= 256 && kblocks % sp == 0 && kblocks / sp >= 4) best = sp;
+  return best;
+}
+
+// Workspace: one 32-bit counter per tile (the counters padded to 256
+// bytes), then `splits` fp32 partial tiles of 128 x 128 per tile.
+int64_t gemm_splitk_workspace(int64_t M, int64_t N, int splits) {
+  if (splits <= 1) return 0;
+  const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+  return (tiles * 4 + 255) / 256 * 256 + tiles * splits * 128 * 128 * 4;
+}
+
+}  // namespace fp8q
+
 namespace {
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -201,6 +231,31 @@ fp8q_status fp8q_gemm(const uint8_t* A, const float* sA, fp8q_granularity gA, in
                       const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
                       void* C, int64_t ldc, struct ihipStream_t* stream) {
   return gemm_checked(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, 0u, C, ldc, stream);
+}
+
+int64_t fp8q_gemm_splitk_workspace(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K <= 0 || M > kMaxDim || N > kMaxDim || K > kMaxDim) return -1;
+  return fp8q::gemm_splitk_workspace(M, N, fp8q::gemm_splitk_splits(M, N, K, K, K, N));
+}
+
+fp8q_status fp8q_gemm_splitk(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda, const uint8_t* B,
+                             const float* sB, fp8q_granularity gB, int64_t ldb, int64_t M, int64_t N, int64_t K,
+                             void* C, int64_t ldc, void* workspace, int64_t workspace_bytes,
+                             struct ihipStream_t* stream) {
+  fp8q::GemmArgs g;
+  int pair = 0;
+  const fp8q_status st = gemm_args(A, sA, gA, lda, B, sB, gB, ldb, M, N, K, 0u, C, ldc, g, pair);
+  if (st != FP8Q_OK) return st;
+  g.splits = fp8q::gemm_splitk_splits(M, N, K, lda, ldb, ldc);
+  if (g.splits > 1) {
+    const int64_t need = fp8q::gemm_splitk_workspace(M, N, g.splits);
+    if (!workspace || workspace_bytes < need) return FP8Q_ERR_INVAL;
+    if (!aligned(workspace, 16)) return FP8Q_ERR_ALIGN;
+    const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    g.cnt = static_cast<uint32_t*>(workspace);
+    g.part = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + (tiles * 4 + 255) / 256 * 256);
+  }
+  return from_hip(fp8q::launch_gemm_splitk(g, pair, reinterpret_cast<hipStream_t>(stream)));
 }
 
 fp8q_status fp8q_gemm_formats(const uint8_t* A, const float* sA, fp8q_granularity gA, int64_t lda,

@@ -345,6 +345,81 @@ __device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t
   if (j < PASSES && m < g.M && n < g.N) g.Cs[(n >> 7) * g.cs_ld + m] = mine.s;
 }
 
+// Split-K reduction.  The g.splits workgroups of one tile each hold the
+// fp32 partial tile of their K range.  Each writes it to its slot of the
+// workspace (slot s of tile t at part + (t * splits + s) * BM * BN floats,
+// every wave's accumulators in register order, lane-interleaved in pairs),
+// then counts itself in cnt[t].  The workgroup that counts last reads the
+// other slots and adds all partials in split order, ((p0 + p1) + p2) + ...,
+// with its own from registers, so the sum does not depend on the order of
+// arrival; it resets cnt[t] to zero for the next call and goes on to the
+// epilogue, the others end.  Visibility across XCDs (each with its own L2)
+// without writing back or invalidating the L2s: the partials are stored
+// and loaded with agent-scope accesses (coherent at the device level), the
+// stores are complete before the count (s_waitcnt), and the loads go out
+// only after the count that found them all.  Returns true in the last
+// workgroup (then `acc` holds the sum).
+template <int TI, int TJ, int TILE_FLOATS>
+__device__ __forceinline__ bool splitk_reduce(const GemmArgs& g, v4f (&acc)[TI][TJ], int split, int tile, int wave,
+                                              int lane, uint8_t* flag_lds) {
+  constexpr int kPairs = TI * TJ * 2;  // 64-bit pairs of accumulators per lane
+  const int S = g.splits;
+  uint64_t* const slab = reinterpret_cast<uint64_t*>(g.part + (int64_t)tile * S * TILE_FLOATS);
+  constexpr int64_t slot_pairs = TILE_FLOATS / 2;
+  auto at = [&](int s, int q) { return slab + s * slot_pairs + ((int64_t)wave * kPairs + q) * 64 + lane; };
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const uint64_t v = (uint64_t)__float_as_uint(acc[i][j][2 * h]) |
+                           ((uint64_t)__float_as_uint(acc[i][j][2 * h + 1]) << 32);
+        __hip_atomic_store(at(split, (i * TJ + j) * 2 + h), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's partial is stored
+  __syncthreads();                                   // and every wave's
+  __attribute__((address_space(3))) uint32_t* const flag = (__attribute__((address_space(3))) uint32_t*)flag_lds;
+  if (threadIdx.x == 0) {
+    const uint32_t before = __hip_atomic_fetch_add(g.cnt + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = before == (uint32_t)(S - 1);
+    if (last) __hip_atomic_store(g.cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last ? 1u : 0u;
+  }
+  __syncthreads();
+  if (*flag == 0u) return false;
+  v4f sum[TI][TJ];
+  for (int s = 0; s < S; ++s) {
+    v4f p[TI][TJ];
+    if (s == split) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) p[i][j] = acc[i][j];
+    } else {
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const uint64_t v = __hip_atomic_load(at(s, (i * TJ + j) * 2 + h), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            p[i][j][2 * h] = __uint_as_float((uint32_t)v);
+            p[i][j][2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
+          }
+    }
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) sum[i][j] = s == 0 ? p[i][j] : sum[i][j] + p[i][j];
+  }
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) acc[i][j] = sum[i][j];
+  return true;
+}
+
 // One workgroup computes a BM x BN tile of C with (BM/WM) x (BN/WN) waves,
 // each owning WM x WN as (WM/16) x (WN/16) MFMA tiles of 16 x 16.  QOUT: the
 // tile leaves as E4M3 codes and 1x128 scales of its bf16 values (see
@@ -354,8 +429,12 @@ __device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t
 // their partial tiles are summed in LDS at the end, group 1 into group 0,
 // then group 2, ... (a fixed order).  Each group's step chain (barrier,
 // fragment reads, MFMAs, FMAs) then overlaps the others' on the same SIMDs.
-template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT, int KS = 1>
-__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
+// SPLITK: the workgroup is split `split` of the g.splits that share tile
+// number `tile`, and sums the K blocks split * KT .. split * KT + KT - 1
+// (KT = K / 128 / g.splits); see splitk_reduce for how the partial tiles
+// meet.
+template <int PAIR, int BM, int BN, int WM, int WN, bool QOUT, int FMT, int KS = 1, bool SPLITK = false>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn, int split = 0, int tile = 0) {
   constexpr int kWavesN = BN / WN;
   constexpr int kWaves = (BM / WM) * kWavesN;  // waves of one group
   constexpr int TI = WM / 16, TJ = WN / 16;
@@ -394,7 +473,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   const int lane = threadIdx.x & 63;
   const int wave = KS > 1 ? uniform(wave_all % kWaves) : wave_all;  // within the group
   const int wm = (wave / kWavesN) * WM, wn = (wave % kWavesN) * WN;
-  const int KT = (int)(g.K / kBK) / KS;  // steps of this group (KS divides K / 128)
+  // steps of this group (KS divides K / 128) or of this split (g.splits
+  // divides it)
+  const int KT = (int)(g.K / kBK) / (SPLITK ? g.splits : KS);
   // K block of the group's step st.  Tiles whose first column lies in an
   // odd 1024-column band walk K backwards: the 256 x 256 row-group raster
   // runs 8 tile rows x 4 tile columns (one band) on an XCD at a time and then the next
@@ -404,7 +485,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
   // so does each sub-problem of a split launch, whose column origins are
   // multiples of 2048 while ldb < 2^20).
   const bool rev = ((n0 >> 10) & 1) != 0;
-  auto kb = [&](int st) { return (rev ? KT - 1 - st : st) * KS + kg; };
+  auto kb = [&](int st) {
+    const int o = rev ? KT - 1 - st : st;
+    return SPLITK ? split * KT + o : o * KS + kg;
+  };
   const int mw = (int)m0 + wm, nw = (int)n0 + wn;  // wave's first row / column
 
   v4f acc[TI][TJ];
@@ -830,6 +914,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int tm, int tn) {
     }
   }
 
+  if constexpr (SPLITK) {
+    static_assert(KS == 1 && !QOUT, "split-K: one group, bf16 output");
+    if (!splitk_reduce<TI, TJ, BM * BN>(g, acc, split, tile, wave, lane, dummy_lds)) return;
+  }
+
   // Epilogue: whole-K scales for tensor / row pairs, bf16 RNE, then the
   // tile goes through LDS (the operand stages are free now) so that global
   // stores are whole 16-byte chunks of contiguous C rows.  LDS row m of the
@@ -916,6 +1005,20 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64 * KS) void gemm_kernel(G
   int tm, tn;
   tile_coords<BM, BN>(g.M, g.N, g.K, blockIdx.x, tm, tn);
   gemm_tile<PAIR, BM, BN, WM, WN, QOUT, FMT, KS>(g, tm, tn);
+}
+
+// Split-K: g.splits workgroups per 128 x 128 tile.  Positions run split by
+// split over the tile raster, so the tiles of one split (which share the A
+// rows of its K range) sit on neighbouring XCDs, and the two tile rows of
+// a 256-row problem that share B rows on one XCD.
+template <int PAIR, int BM, int BN, int WM, int WN, int FMT>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_splitk_kernel(GemmArgs g) {
+  const int tiles = (int)((g.M + BM - 1) / BM) * (int)((g.N + BN - 1) / BN);
+  const int id = xcd_order(tiles * g.splits, blockIdx.x);
+  const int split = id / tiles, t = id - split * tiles;
+  int tm, tn;
+  raster<BM, BN>(g.M, g.N, g.K, t, tm, tn);
+  gemm_tile<PAIR, BM, BN, WM, WN, false, FMT, 1, true>(g, tm, tn, split, t);
 }
 
 // Grouped GEMM: one launch over several problems that share the pair, the
@@ -1081,6 +1184,12 @@ FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 1)
 FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 2)
 FP8Q_GEMM_KERNEL_KS2(kPairBlockK, 3)
 #undef FP8Q_GEMM_KERNEL_KS2
+#define FP8Q_GEMM_SPLITK(PAIR) template __global__ void gemm_splitk_kernel<PAIR, 128, 128, 32, 64, 0>(GemmArgs);
+FP8Q_GEMM_SPLITK(kPairTensor)
+FP8Q_GEMM_SPLITK(kPairRow)
+FP8Q_GEMM_SPLITK(kPairBlock)
+FP8Q_GEMM_SPLITK(kPairBlockK)
+#undef FP8Q_GEMM_SPLITK
 template __global__ void gemm_kernel<kPairBlock, 256, 256, 128, 64, true, 0>(GemmArgs);
 template __global__ void gemm_kernel<kPairBlock, 128, 128, 64, 64, true, 0>(GemmArgs);
 #define FP8Q_GEMM_GROUPED(PAIR)                                                     \
@@ -1188,6 +1297,22 @@ hipError_t launch_gemm_grouped(const GemmGroup& gs, int pair, hipStream_t s) {
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s) {
   if (pair != kPairBlock || g.N % 128) return hipErrorInvalidValue;
   return launch_split<kPairBlock, true, 0>(g, s);
+}
+
+hipError_t launch_gemm_splitk(const GemmArgs& g, int pair, hipStream_t s) {
+  if (g.splits <= 1) return launch_gemm(g, pair, 0, s);
+  const int64_t tiles = ((g.M + 127) / 128) * ((g.N + 127) / 128);
+  if (!g.part || !g.cnt || g.splits > 8 || (g.K / kBK) % g.splits || tiles * g.splits > 256)
+    return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(tiles * g.splits));
+  switch (pair) {
+    case kPairTensor: gemm_splitk_kernel<kPairTensor, 128, 128, 32, 64, 0><<<grid, 512, 0, s>>>(g); break;
+    case kPairRow: gemm_splitk_kernel<kPairRow, 128, 128, 32, 64, 0><<<grid, 512, 0, s>>>(g); break;
+    case kPairBlock: gemm_splitk_kernel<kPairBlock, 128, 128, 32, 64, 0><<<grid, 512, 0, s>>>(g); break;
+    case kPairBlockK: gemm_splitk_kernel<kPairBlockK, 128, 128, 32, 64, 0><<<grid, 512, 0, s>>>(g); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace fp8q

@@ -55,6 +55,12 @@ struct GemmArgs {
   uint8_t* Cq;
   float* Cs;
   int64_t ldq, cs_ld;
+  // split-K (fp8q_gemm_splitk): `splits` workgroups share a tile, each
+  // summing a contiguous range of K blocks; their fp32 partial tiles go to
+  // `part` and the last to arrive (counted in cnt[tile]) adds them up
+  float* part = nullptr;
+  uint32_t* cnt = nullptr;
+  int splits = 1;
 };
 
 // kPairBlockE8: 1x128 x 128x128 with power-of-two scales (applied inside
@@ -78,6 +84,13 @@ struct GemmGroup {
 // (else hipErrorInvalidValue; the C-ABI checks them first).
 hipError_t launch_gemm_grouped(const GemmGroup& gs, int pair, hipStream_t s);
 hipError_t launch_gemm_quantized(const GemmArgs& g, int pair, hipStream_t s);
+
+// Split-K for skinny problems: the number of workgroups per 128 x 128 tile
+// (1: no split, the call is launch_gemm's) and the workspace bytes it needs.
+int gemm_splitk_splits(int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc);
+int64_t gemm_splitk_workspace(int64_t M, int64_t N, int splits);
+// g.part / g.cnt / g.splits set from a workspace of that size
+hipError_t launch_gemm_splitk(const GemmArgs& g, int pair, hipStream_t s);
 
 // Calibrated Clipping: per-token float32 arrays of n tokens, the grids
 // l_min + k step (k < nl) and h_min + k step (k < nh), and a workspace of

@@ -122,6 +122,49 @@ int main() {
                              codes, BIG, scales, nullptr),
          FP8Q_ERR_UNSUPPORTED, 0);
 
+  // split-K: sizes, the split count and where the counters and partials go
+  {
+    const int64_t ws_down = fp8q_gemm_splitk_workspace(256, 4096, 12288);
+    if (ws_down != 256 + 64 * 4 * 65536) {
+      fprintf(stderr, "split-K workspace %lld\n", (long long)ws_down);
+      ++failures;
+    }
+    EXPECT(fp8q_gemm_splitk_workspace(256, 12288, 4096), 0, 0);
+    EXPECT(fp8q_gemm_splitk_workspace(0x7fffffff, 0x7fffffff, 0x7fffff80), 0, 0);
+    EXPECT(fp8q_gemm_splitk_workspace(BIG, BIG, BIG), -1, 0);
+    EXPECT(fp8q_gemm_splitk_workspace(0, 128, 1024), -1, 0);
+    EXPECT(fp8q_gemm_splitk_workspace(HUGE_DIM, 128, 1024), -1, 0);
+    uint8_t* ws = fake<uint8_t>(1 << 20);
+    EXPECT(fp8q_gemm_splitk(cA, sA, FP8Q_BLOCK_1x128, 12288, cA, sA, FP8Q_BLOCK_128x128, 12288, 256, 4096, 12288, C,
+                            4096, ws, ws_down, nullptr),
+           FP8Q_OK, 1);
+    if (fp8q::stub_gemm.splits != 4 || (void*)fp8q::stub_gemm.cnt != (void*)ws ||
+        (void*)fp8q::stub_gemm.part != (void*)(ws + 256)) {
+      fprintf(stderr, "split-K arguments: splits %d\n", fp8q::stub_gemm.splits);
+      ++failures;
+    }
+    EXPECT(fp8q_gemm_splitk(cA, sA, FP8Q_BLOCK_1x128, 12288, cA, sA, FP8Q_BLOCK_128x128, 12288, 256, 4096, 12288, C,
+                            4096, ws, ws_down - 1, nullptr),
+           FP8Q_ERR_INVAL, 0);
+    EXPECT(fp8q_gemm_splitk(cA, sA, FP8Q_BLOCK_1x128, 12288, cA, sA, FP8Q_BLOCK_128x128, 12288, 256, 4096, 12288, C,
+                            4096, nullptr, ws_down, nullptr),
+           FP8Q_ERR_INVAL, 0);
+    EXPECT(fp8q_gemm_splitk(cA, sA, FP8Q_BLOCK_1x128, 12288, cA, sA, FP8Q_BLOCK_128x128, 12288, 256, 4096, 12288, C,
+                            4096, ws + 8, ws_down, nullptr),
+           FP8Q_ERR_ALIGN, 0);
+    // not split: no workspace needed, fp8q_gemm's launch with splits = 1
+    EXPECT(fp8q_gemm_splitk(cA, sA, FP8Q_BLOCK_1x128, 4096, cA, sA, FP8Q_BLOCK_128x128, 4096, 256, 12288, 4096, C,
+                            12288, nullptr, 0, nullptr),
+           FP8Q_OK, 1);
+    if (fp8q::stub_gemm.splits != 1) {
+      fprintf(stderr, "unsplit call: splits %d\n", fp8q::stub_gemm.splits);
+      ++failures;
+    }
+    EXPECT(fp8q_gemm_splitk(cA, sA, FP8Q_BLOCK_1x128, BIG, cA, sA, FP8Q_BLOCK_128x128, BIG, BIG, BIG, 4096, C, BIG,
+                            ws, ws_down, nullptr),
+           FP8Q_ERR_UNSUPPORTED, 0);
+  }
+
   // grouped
   fp8q_gemm_problem p[FP8Q_MAX_GROUP + 1];
   for (auto& q : p) q = fp8q_gemm_problem{cA, sA, 4096, cA, sA, 4096, C, 6144, 16384, 6144};

@@ -42,6 +42,12 @@ hipError_t launch_gemm_quantized(const GemmArgs& g, int, hipStream_t) {
   stub_gemm = g;
   return hipSuccess;
 }
+hipError_t launch_gemm_splitk(const GemmArgs& g, int pair, hipStream_t) {
+  ++stub_calls;
+  stub_gemm = g;
+  stub_pair = pair;
+  return hipSuccess;
+}
 // the real slot counts of the two instantiations of the clipping kernels
 int clip_slots(int nl, int nh) {
   if (nl <= 21 && nh <= 41) return 5 + 2 * 22 + 42;

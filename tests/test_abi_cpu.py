@@ -118,6 +118,37 @@ def test_gemm_rejections(L):
     assert gemm(L, ldc=258) == -3
 
 
+def gemm_sk(L, ws=FAKE, ws_bytes=1 << 30, **kw):
+    args = dict(A=FAKE, sA=FAKE, gA=3, lda=12288, B=FAKE, sB=FAKE, gB=5, ldb=12288, M=256, N=4096, K=12288,
+                C=FAKE, ldc=4096)
+    args.update(kw)
+    return L.fp8q_gemm_splitk(*args.values(), ws, ws_bytes, None)
+
+
+def test_gemm_splitk_workspace_sizes(L):
+    """Split counts: the largest power of two up to 8 with tiles x S <= 256
+    and at least four K blocks per split; the workspace is one counter per
+    tile padded to 256 bytes, then S fp32 128 x 128 partial tiles per tile."""
+    ws = L.fp8q_gemm_splitk_workspace
+    assert ws(256, 4096, 12288) == 256 + 64 * 4 * 128 * 128 * 4       # decode down: 64 tiles, S = 4
+    assert ws(256, 12288, 4096) == 0                                   # 192 tiles: not split
+    assert ws(200, 384, 1024) == 256 + 6 * 2 * 65536                   # 8 K blocks: S = 2
+    assert ws(200, 384, 2048) == 256 + 6 * 4 * 65536
+    assert ws(200, 384, 4096) == 256 + 6 * 8 * 65536
+    assert ws(128, 128, 384) == 0                                      # 3 K blocks
+    assert ws(128, 128, 200) == 0                                      # K not whole blocks
+    assert ws(0, 128, 1024) == -1 and ws(128, -1, 1024) == -1 and ws(128, 128, 1 << 31) == -1
+
+
+def test_gemm_splitk_rejections(L):
+    assert gemm_sk(L, A=None) == -1
+    assert gemm_sk(L, gA=3, gB=4) == -2
+    assert gemm_sk(L, ws=None) == -1                                  # splits and needs one
+    assert gemm_sk(L, ws_bytes=L.fp8q_gemm_splitk_workspace(256, 4096, 12288) - 1) == -1
+    assert gemm_sk(L, ws=FAKE + 8) == -3
+    assert gemm_sk(L, C=FAKE + 2) == -3
+
+
 def test_gemm_pow2_rejections(L):
     def gp(**kw):
         args = dict(A=FAKE, sA=FAKE, gA=3, lda=256, B=FAKE, sB=FAKE, gB=5, ldb=256, M=256, N=256, K=256,

@@ -48,23 +48,25 @@ def oracle_operand(x, g, transposed=False):
     return _par.quantize(synth.bf16_bits(x), g, transposed)
 
 
-def run_pair(a_src, b_src, ga, gb, a_t=False, b_t=False, rows=None, label="", pad=0):
+def run_pair(a_src, b_src, ga, gb, a_t=False, b_t=False, rows=None, label="", pad=0, gemm=None, adds=1):
     """a_src, b_src: bf16 CUDA tensors whose quantization (optionally
     transposed) gives A [M, K] and B [N, K].  Checks the listed rows of C (all
     rows by default) against the oracle; returns the error.  pad > 0: C is
     the first N columns of a [M, N + pad] buffer whose other columns must
-    stay untouched."""
+    stay untouched.  gemm: the entry point (fp8q.gemm by default); adds: the
+    fp32 additions of partial tiles it makes beyond one (window_check)."""
+    gemm = gemm or fp8q.gemm
     print("gemm parity", label, tuple(a_src.shape), tuple(b_src.shape), ga, gb, flush=True)
     A, sA = gpu_operand(a_src, ga if not a_t else fp8q.BLOCK_128x1, a_t)
     B, sB = gpu_operand(b_src, gb if not b_t else (fp8q.BLOCK_128x1 if gb == fp8q.BLOCK_1x128 else gb), b_t)
     if pad:
         buf = torch.full((A.shape[0], B.shape[0] + pad), -7.0, dtype=torch.bfloat16, device=DEV)
-        C = fp8q.gemm(A, sA, ga, B, sB, gb, out=buf[:, :B.shape[0]])
+        C = gemm(A, sA, ga, B, sB, gb, out=buf[:, :B.shape[0]])
         torch.cuda.synchronize()
         assert torch.all(buf[:, B.shape[0]:] == -7.0), "columns past N were written"
         del buf
     else:
-        C = fp8q.gemm(A, sA, ga, B, sB, gb)
+        C = gemm(A, sA, ga, B, sB, gb)
     torch.cuda.synchronize()
     M = A.shape[0]
     if rows is None:
@@ -88,7 +90,7 @@ def run_pair(a_src, b_src, ga, gb, a_t=False, b_t=False, rows=None, label="", pa
     kind = "accumulate" if ga in (fp8q.TENSOR, fp8q.ROW) else "promote"
     a_rows = oA[rows] if ga == fp8q.TENSOR else oA
     return _par.check_gemm(got, ref, a_rows, osA, ga, oB, osB, gb, kind, tol=TOL,
-                           tol_rms_floor=TOL_ELEMENTWISE, label=label)
+                           tol_rms_floor=TOL_ELEMENTWISE, label=label, adds=adds)
 
 
 @pytest.mark.parametrize("pair", list(PAIRS))
@@ -164,7 +166,7 @@ def test_dgrad_layout_small():
     run_pair(dy, w, fp8q.BLOCK_1x128, fp8q.BLOCK_128x128, b_t=True, label="dgrad small")
 
 
-def identity_case(ga, gb, M=160, K=256):
+def identity_case(ga, gb, M=160, K=256, gemm=None):
     """B = identity codes (0x38 = 1.0) with power-of-two scales; every A
     block's amax is 448 * 2^k so S_A = 2^k exactly.  Every output is a single
     exact product, so C must equal S_A * S_B * decode(A) bit for bit."""
@@ -187,7 +189,7 @@ def identity_case(ga, gb, M=160, K=256):
     B[torch.arange(N), torch.arange(K)] = 0x38
     nb = fp8q.scales_count(N, K, gb)
     sB = torch.from_numpy((2.0 ** rng.integers(-4, 4, size=nb)).astype(np.float32)).to(DEV)
-    C = fp8q.gemm(A, sA, ga, B, sB, gb)
+    C = (gemm or fp8q.gemm)(A, sA, ga, B, sB, gb)
     torch.cuda.synchronize()
     # expected from the oracle's own quantization of the same bf16 input
     oA, osA = oracle.quantize(synth.bf16_bits(a), ga)
