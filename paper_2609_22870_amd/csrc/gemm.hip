@@ -349,10 +349,10 @@ __device__ __forceinline__ void store_quantized(const GemmArgs& g, const uint8_t
 // fp32 partial tile of their K range.  Each writes it to its slot of the
 // workspace (slot s of tile t at part + (t * splits + s) * BM * BN floats,
 // every wave's accumulators in register order, lane-interleaved in pairs),
-// then counts itself in cnt[t].  The workgroup that counts last reads the
-// other slots and adds all partials in split order, ((p0 + p1) + p2) + ...,
-// with its own from registers, so the sum does not depend on the order of
-// arrival; it resets cnt[t] to zero for the next call and goes on to the
+// then counts itself in cnt[t].  The workgroup that counts last reads all
+// the slots back and adds the partials in split order, ((p0 + p1) + p2) +
+// ..., so the sum does not depend on the order of arrival; it resets
+// cnt[t] to zero for the next call and goes on to the
 // epilogue, the others end.  Visibility across XCDs (each with its own L2)
 // without writing back or invalidating the L2s: the partials are stored
 // and loaded with agent-scope accesses (coherent at the device level), the
@@ -388,15 +388,15 @@ __device__ __forceinline__ bool splitk_reduce(const GemmArgs& g, v4f (&acc)[TI][
   }
   __syncthreads();
   if (*flag == 0u) return false;
+  // every slot is read back (this workgroup's own too: the same bits it
+  // holds), four at a time with all their loads in flight, and added in
+  // split order; slots past S repeat the last one and are not added
   v4f sum[TI][TJ];
-  for (int s = 0; s < S; ++s) {
-    v4f p[TI][TJ];
-    if (s == split) {
+  for (int s0 = 0; s0 < S; s0 += 4) {
+    v4f p[4][TI][TJ];
 #pragma unroll
-      for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j) p[i][j] = acc[i][j];
-    } else {
+    for (int u = 0; u < 4; ++u) {
+      const int s = s0 + u < S ? s0 + u : S - 1;
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
@@ -404,14 +404,19 @@ __device__ __forceinline__ bool splitk_reduce(const GemmArgs& g, v4f (&acc)[TI][
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
             const uint64_t v = __hip_atomic_load(at(s, (i * TJ + j) * 2 + h), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            p[i][j][2 * h] = __uint_as_float((uint32_t)v);
-            p[i][j][2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
+            p[u][i][j][2 * h] = __uint_as_float((uint32_t)v);
+            p[u][i][j][2 * h + 1] = __uint_as_float((uint32_t)(v >> 32));
           }
     }
 #pragma unroll
-    for (int i = 0; i < TI; ++i)
+    for (int u = 0; u < 4; ++u) {
+      if (s0 + u < S) {
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) sum[i][j] = s == 0 ? p[i][j] : sum[i][j] + p[i][j];
+        for (int i = 0; i < TI; ++i)
+#pragma unroll
+          for (int j = 0; j < TJ; ++j) sum[i][j] = s0 + u == 0 ? p[u][i][j] : sum[i][j] + p[u][i][j];
+      }
+    }
   }
 #pragma unroll
   for (int i = 0; i < TI; ++i)
