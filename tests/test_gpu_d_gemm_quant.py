@@ -18,6 +18,9 @@ activation operand straight out of the GEMM.  Calls go through the C-ABI.
   the E4M3 rounding (2^-4 of the value) per row.
 * The fused kernel also gives exactly the bytes of fp8q_gemm followed by
   fp8q_quantize (a consistency check between two entry points)."""
+import ctypes
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -30,6 +33,7 @@ import _par
 
 pytestmark = pytest.mark.gpu
 
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 DEV = "cuda:0"
 TOL_DEQ = 2.0 ** -4 + 5e-3
 
@@ -127,16 +131,6 @@ def bf16_neighbours(lo, hi):
     return b_lo, b_hi, b_lo == b_hi
 
 
-def next_bf16_up(v):
-    """The bf16 value after v (toward +inf), float64 in and out."""
-    f = np.asarray(v, dtype=np.float32)
-    u = (f.view(np.uint32) >> 16).astype(np.int64)
-    neg = u >= 0x8000
-    up = np.where(f == 0, 1, np.where(neg, u - 1, u + 1))
-    up = np.where((f == 0) & neg, 1, up)
-    return (up.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-
-
 def check_units(got, gs, oA, osA, oB, osB, K):
     """got: GPU codes [rows, N]; gs: GPU scales [rows, N/128]."""
     rows, N = got.shape
@@ -153,25 +147,31 @@ def check_units(got, gs, oA, osA, oB, osB, K):
     bad = np.argwhere(unit_fixed & ~(code_ok & scale_ok))
     assert bad.shape[0] == 0, "%d fixed units differ, first (row, unit) %s" % (bad.shape[0], bad[:4].tolist())
     # other units: a possible amax's scale, and each code the cast of one of
-    # its element's possible bf16 values with that scale (at most a few)
-    for r, u in np.argwhere(~unit_fixed):
-        sl = slice(u * 128, (u + 1) * 128)
-        cands = [b_lo[r, sl]]
-        while True:
-            nxt = np.minimum(next_bf16_up(cands[-1]), b_hi[r, sl])
-            if np.array_equal(nxt, cands[-1]):
-                break
-            cands.append(nxt)
-        mags = np.abs(np.stack(cands))
-        amax_lo, amax_hi = np.max(np.min(mags, axis=0)), np.max(np.max(mags, axis=0))
-        s_lo = np.float32(np.float32(amax_lo) / np.float32(448.0))
-        s_hi = np.float32(np.float32(amax_hi) / np.float32(448.0))
-        s_gpu = gs[r, u]
-        assert s_lo <= s_gpu <= s_hi, (r, u, s_lo, s_gpu, s_hi)
-        ok = np.zeros(128, dtype=bool)
-        for c in cands:
-            ok |= oracle.cast_f32(c.astype(np.float32), float(s_gpu)) == got[r, sl]
-        assert ok.all(), (r, u, np.argwhere(~ok)[:4].tolist())
+    # its element's possible bf16 values with that scale (tests/csrc/unit_check.c)
+    check = np.ascontiguousarray(~unit_fixed, dtype=np.uint8)
+    first = np.zeros(3, dtype=np.int64)
+    ptr = lambda a: a.ctypes.data_as(ctypes.c_void_p)
+    lo_bits = np.ascontiguousarray(to_bf16_bits(b_lo))
+    hi_bits = np.ascontiguousarray(to_bf16_bits(b_hi))
+    got_c = np.ascontiguousarray(got, dtype=np.uint8)
+    gs_c = np.ascontiguousarray(gs, dtype=np.float32)
+    n_bad = _unit_check()(ptr(lo_bits), ptr(hi_bits), ptr(got_c), ptr(gs_c), ptr(check), rows, N, ptr(first))
+    assert n_bad == 0, "%d unfixed units fail, first (row, unit, 1 scale / 2 code) %s" % (n_bad, first.tolist())
+
+
+_UNIT_CHECK = None
+
+
+def _unit_check():
+    global _UNIT_CHECK
+    if _UNIT_CHECK is None:
+        from _cbuild import helper
+        L = helper("unit_check", link_oracle=True, extra=["-I", os.path.join(ROOT, "oracle")])
+        p, i64 = ctypes.c_void_p, ctypes.c_int64
+        L.unit_check.argtypes = [p, p, p, p, p, i64, i64, p]
+        L.unit_check.restype = i64
+        _UNIT_CHECK = L.unit_check
+    return _UNIT_CHECK
 
 
 def test_small_several_tiles_ragged():
