@@ -102,7 +102,7 @@ static i128 pair_sum(const uint8_t *a, const uint8_t *b, int64_t k0, const int64
  * the same truncations; the results are equal to pair_sum's. */
 static int64_t trunc_to64(int64_t p, int s) {
   if (s <= 0) return p;
-  if (s >= 62) return 0; /* not reached: narrow products stay below 2^55 units */
+  if (s >= 62) return 0; /* not reached by the narrow formats */
   const int64_t m = p < 0 ? -p : p;
   const int64_t t = (m >> s) << s;
   return p < 0 ? -t : t;
@@ -110,13 +110,13 @@ static int64_t trunc_to64(int64_t p, int s) {
 
 static int64_t floor_to64(int64_t p, int s) {
   if (s <= 0) return p;
-  if (s >= 62) return p < 0 ? INT64_MIN / 4 : 0; /* not reached: narrow sums stay below 2^55 units */
+  if (s >= 62) return p < 0 ? INT64_MIN / 4 : 0; /* not reached by the narrow formats */
   return (p >> s) << s;
 }
 
 /* One pair in the narrow form, on operands decoded beforehand: value v (in
  * units of 2^-shift) and exponent e per K index (e of the table in use). */
-static int64_t pair_sum64(const int32_t *av, const int16_t *ae, const int32_t *bv, const int16_t *be, int64_t k0,
+static int64_t pair_sum64(const int64_t *av, const int16_t *ae, const int64_t *bv, const int16_t *be, int64_t k0,
                           int base, int *have_out) {
   int64_t sums[2] = {0, 0};
   int have[2] = {0, 0}, E[2] = {0, 0};
@@ -129,7 +129,7 @@ static int64_t pair_sum64(const int32_t *av, const int16_t *ae, const int32_t *b
       have[h] = 1;
     }
     if (!have[h]) continue;
-    for (int k = 0; k < 8; ++k) sums[h] += trunc_to64((int64_t)av[g0 + k] * bv[g0 + k], E[h] - 13 + base);
+    for (int k = 0; k < 8; ++k) sums[h] += trunc_to64(av[g0 + k] * bv[g0 + k], E[h] - 13 + base);
   }
   *have_out = have[0] || have[1];
   if (!*have_out) return 0;
@@ -142,13 +142,13 @@ static int64_t pair_sum64(const int32_t *av, const int16_t *ae, const int32_t *b
  * subnormal (only then can the two exponent tables give different pair
  * sums). */
 typedef struct {
-  int32_t *v;
+  int64_t *v;
   int16_t *e, *f;
   uint8_t *sub;
 } decoded_t;
 
 static int decoded_alloc(decoded_t *d, int64_t K) {
-  d->v = malloc(K * sizeof(int32_t));
+  d->v = malloc(K * sizeof(int64_t));
   d->e = malloc(K * sizeof(int16_t));
   d->f = malloc(K * sizeof(int16_t));
   d->sub = malloc(K / 16);
@@ -165,7 +165,7 @@ static void decoded_free(decoded_t *d) {
 static void decode_row(const uint8_t *c, int64_t K, const int64_t *v, const int32_t *e, const int32_t *f,
                        decoded_t *d) {
   for (int64_t k = 0; k < K; ++k) {
-    d->v[k] = (int32_t)v[c[k]];
+    d->v[k] = v[c[k]];
     d->e[k] = (int16_t)e[c[k]];
     d->f[k] = (int16_t)f[c[k]];
   }
@@ -211,8 +211,9 @@ static void element_wide(const job_t *j, int64_t r, int64_t n) {
   j->slack[r * j->N + n] = (double)slack;
 }
 
-/* The same for formats whose products and sums fit 62 bits, on decoded
- * rows, in 64-bit integers: the same values as element_wide. */
+/* The same for format pairs whose products and block sums fit 62 bits
+ * (E4M3 x E4M3, E4M3 x E5M2), on decoded rows, in 64-bit integers: the
+ * same values as element_wide. */
 static void element_narrow(const job_t *j, int64_t r, int64_t n, const decoded_t *da, const decoded_t *db) {
   const int64_t K = j->K, KB = K / 128;
   const int base = j->shift_a + j->shift_b;
@@ -229,7 +230,7 @@ static void element_narrow(const job_t *j, int64_t r, int64_t n, const decoded_t
       blk += v;
       blk_slack += f > v ? f - v : v - f;
       for (int k = 0; k < 16; ++k) {
-        const int64_t p = (int64_t)da->v[k0 + k] * db->v[k0 + k];
+        const int64_t p = da->v[k0 + k] * db->v[k0 + k];
         blk_abs += p < 0 ? -p : p;
       }
     }
@@ -252,10 +253,9 @@ static void *work(void *arg) {
     if (x > max_a) max_a = x;
     if (y > max_b) max_b = y;
   }
-  /* every value fits int32, and every product, group, pair and block sum
-   * stays below 2^55 units */
-  int narrow = max_a < ((int64_t)1 << 31) && max_b < ((int64_t)1 << 31) &&
-               (double)max_a * (double)max_b * 128.0 < 36028797018963968.0;
+  /* every product, group, pair and block sum stays below 2^62 units, so
+   * every truncation shift stays below 62 */
+  int narrow = (double)max_a * (double)max_b * 128.0 < 4611686018427387904.0;
   decoded_t db, *da = NULL;
   const int64_t rows = j->r1 - j->r0;
   if (narrow) {
