@@ -137,3 +137,44 @@ def test_unsplit_problem_is_fp8q_gemm():
     want = fp8q.gemm(A, sA, fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128)
     torch.cuda.synchronize()
     assert torch.equal(got.view(torch.int16), want.view(torch.int16))
+
+
+def test_graph_replays_and_side_stream():
+    """Captured in a HIP graph (no memset inside: the counters reset
+    themselves) and replayed three times, with eager calls of another shape
+    through the same workspace, on a stream of their own, in between: every
+    replay gives the eager result bit for bit, and the counters are zero
+    after each."""
+    M, K, N = 256, 12288, 4096
+    A, sA, B, sB = _operands(M, K, N, seed=970)
+    A2, sA2, B2, sB2 = _operands(200, 4096, 384, seed=980)
+    need = max(fp8q.gemm_splitk_workspace(M, N, K), fp8q.gemm_splitk_workspace(200, 384, 4096))
+    ws = torch.zeros(need, dtype=torch.uint8, device=DEV)
+    eager = fp8q.gemm_splitk(A, sA, fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128, workspace=ws)
+    torch.cuda.synchronize()
+    out = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            fp8q.gemm_splitk(A, sA, fp8q.BLOCK_1x128, B, sB, fp8q.BLOCK_128x128, out=out, workspace=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    tiles = ((M + 127) // 128) * ((N + 127) // 128)
+    for rep in range(3):
+        print("split-K graph replay", rep, flush=True)
+        out.fill_(7.0)
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), rep
+        assert int(ws[:4 * tiles].count_nonzero()) == 0
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            other = fp8q.gemm_splitk(A2, sA2, fp8q.BLOCK_1x128, B2, sB2, fp8q.BLOCK_128x128, workspace=ws)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        want = fp8q.gemm_splitk(A2, sA2, fp8q.BLOCK_1x128, B2, sB2, fp8q.BLOCK_128x128)
+        torch.cuda.synchronize()
+        assert torch.equal(other.view(torch.int16), want.view(torch.int16)), rep
