@@ -178,3 +178,16 @@ def test_graph_replays_and_side_stream():
         want = fp8q.gemm_splitk(A2, sA2, fp8q.BLOCK_1x128, B2, sB2, fp8q.BLOCK_128x128)
         torch.cuda.synchronize()
         assert torch.equal(other.view(torch.int16), want.view(torch.int16)), rep
+
+
+@pytest.mark.parametrize("pair", ["tensor", "row"])
+def test_splitk_padded_output(pair):
+    """C as the first N columns of a wider buffer (ldc = N + 6, so C rows are
+    only 8-byte aligned and the 8-byte store path runs), N not a multiple of
+    4: the columns past N stay untouched, the rest match the oracle."""
+    ga, gb = PAIRS[pair]
+    M, K, N = 200, 2048, 390
+    a = synth.activations(M, K, seed=991, outlier_seed=992, device=DEV)
+    b = synth.weights(N, K, seed=993, device=DEV)
+    assert splits_of(M, N, K) == 4
+    tb.run_pair(a, b, ga, gb, label="split-K padded " + pair, pad=6, gemm=fp8q.gemm_splitk, adds=3)
