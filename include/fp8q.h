@@ -273,9 +273,8 @@ int64_t fp8q_gemm_splitk_workspace(int64_t M, int64_t N, int64_t K);
 /*
  * fp8q_gemm for skinny problems such as a decode step of the FP8 rollout
  * (Sec. 2.3, Sec. 5: a few hundred rows of activations against a full
- * weight), where
- * the 128 x 128 tiles of C are too few to give every CU one (fewer than
- * 128).  The K blocks of each tile are split over S workgroups (S a power
+ * weight), where the 128 x 128 tiles of C are too few to give every CU one
+ * (fewer than 128).  The K blocks of each tile are split over S workgroups (S a power
  * of two up to 8, S x tiles <= 256, at least four K blocks each), so that
  * each CU streams 1/S of the tile's operand rows; the S fp32 partial tiles
  * are added in a fixed order, then rounded to bf16 once.  The product,
